@@ -1,0 +1,170 @@
+"""Oracle: Maximizing Differential Advantage Pruning + stream compaction
+(test infrastructure only; see oracle/__init__).
+
+Paper, Sec. 3.2 and Alg. 1 Phase 2:
+* partition a question's rollouts by advantage value (Eq. grouping);
+* token n-gram Jaccard distance theta_ij = 1 - |N_n(o_i) & N_n(o_j)| / |N_n(o_i) | N_n(o_j)|
+  where N_n(o) is the set of distinct contiguous n-grams of o's tokens;
+* inside each class, traverse the members and keep o_i unless some already-kept
+  o_j of the same class has theta_ij < tau (strict), i.e. a greedy maximal
+  independent set of the conflict graph {theta < tau};
+* the kept set of the question is the union over classes.
+
+Readings where the paper is silent or ambiguous:
+* traversal order inside a class: Alg. 1 orders by |A_i| descending, which is
+  constant inside a class, so ties are broken by ascending trajectory index;
+* tau is a rational tau_num / tau_den and the comparison is done exactly
+  (``fractions.Fraction``); theta of two empty n-gram sets is 0, and of one empty
+  and one non-empty set is 1 (the definition with |union| > 0);
+* keep-ratio budget (not in the paper; the workload fixes a keep ratio rho):
+  K_q = clamp(floor(rho * G_q + 0.5), 1, G_q).  Classes are ordered by
+  kappa_k = |G_q * r_k - sum_j r_j| descending (proportional to |A| of the class;
+  the sum runs over the question's rewards in index order in float64), ties by
+  lowest first member.  The priority list is a round-robin over the ordered
+  classes taking each class's next MDAP-kept member (ascending index); once those
+  run out, the round-robin continues over the MDAP-pruned members.  The first K_q
+  entries are kept.  rho = 0 means pure MDAP.
+* questions marked invalid (DAPO drop of all-equal groups) keep nothing and report
+  an MDAP count of 0.
+"""
+from fractions import Fraction
+import math
+
+import numpy as np
+
+
+def ngram_set(tokens, n):
+    """N_n(o): the set of distinct contiguous n-grams (as tuples) of a token list."""
+    toks = [int(t) for t in tokens]
+    return {tuple(toks[i:i + n]) for i in range(len(toks) - n + 1)}
+
+
+def jaccard_counts(si, sj):
+    """(|si & sj|, |si | sj|) of two n-gram sets."""
+    inter = len(si & sj)
+    return inter, len(si) + len(sj) - inter
+
+
+def theta_below_tau(inter, union, tau_num, tau_den):
+    """theta < tau, exactly, with theta = 1 - inter/union (0 when union == 0)."""
+    theta = Fraction(union - inter, union) if union > 0 else Fraction(0)
+    return theta < Fraction(tau_num, tau_den)
+
+
+def greedy_mdap_class(members, sets, tau_num, tau_den):
+    """S'_k: traverse ``members`` (ascending index) and keep o_i unless some kept
+    o_j has theta_ij < tau.  ``sets`` maps member -> n-gram set."""
+    kept = []
+    for i in members:
+        conflict = False
+        for j in kept:
+            inter, union = jaccard_counts(sets[i], sets[j])
+            if theta_below_tau(inter, union, tau_num, tau_den):
+                conflict = True
+                break
+        if not conflict:
+            kept.append(i)
+    return kept
+
+
+def class_kappa(rewards_q, cls_q):
+    """kappa per class id: |G * r_k - sum_j r_j| in float64, sum in index order."""
+    G = len(rewards_q)
+    s = 0.0
+    for r in rewards_q:
+        s += float(r)
+    kap = {}
+    for r, c in zip(rewards_q, cls_q):
+        if c not in kap:
+            kap[c] = abs(float(G) * float(r) - s)
+    return kap
+
+
+def budget_size(G, keep_ratio):
+    """K_q = clamp(floor(rho * G + 0.5), 1, G) in float64."""
+    k = int(math.floor(float(keep_ratio) * float(G) + 0.5))
+    return max(1, min(G, k))
+
+
+def budget_keep(rewards_q, cls_q, mdap_keep_q, keep_ratio):
+    """Apply the keep-ratio budget to one question.  Returns a bool list."""
+    G = len(rewards_q)
+    kap = class_kappa(rewards_q, cls_q)
+    first = {}
+    for i, c in enumerate(cls_q):
+        first.setdefault(c, i)
+    order = sorted(kap.keys(), key=lambda c: (-kap[c], first[c]))
+    priority = []
+    for tier in (True, False):
+        lists = [[i for i in range(G) if cls_q[i] == c and bool(mdap_keep_q[i]) == tier]
+                 for c in order]
+        rnd = 0
+        while any(rnd < len(l) for l in lists):
+            for l in lists:
+                if rnd < len(l):
+                    priority.append(l[rnd])
+            rnd += 1
+    K = budget_size(G, keep_ratio)
+    keep = [False] * G
+    for i in priority[:K]:
+        keep[i] = True
+    return keep
+
+
+def prune_prompt(tokens_q, rewards_q, cls_q, ngram_n, tau_num, tau_den, keep_ratio,
+                 valid=True):
+    """One question.  Returns (keep bool[G], mdap_count)."""
+    G = len(rewards_q)
+    if not valid:
+        return [False] * G, 0
+    sets = [ngram_set(t, ngram_n) for t in tokens_q]
+    mdap = [False] * G
+    for c in sorted(set(cls_q)):
+        members = [i for i in range(G) if cls_q[i] == c]
+        for i in greedy_mdap_class(members, sets, tau_num, tau_den):
+            mdap[i] = True
+    count = sum(mdap)
+    if keep_ratio > 0:
+        return budget_keep(rewards_q, cls_q, mdap, keep_ratio), count
+    return mdap, count
+
+
+def prune_batch(token_ids, traj_tok_off, rewards, group_off, class_id, group_valid,
+                ngram_n=1, tau_num=4, tau_den=5, keep_ratio=0.0):
+    """Whole batch.  Returns (keep_mask uint8[N], mdap_count int32[Q])."""
+    tok = np.asarray(token_ids)
+    toff = np.asarray(traj_tok_off, dtype=np.int64)
+    r32 = np.asarray(rewards, dtype=np.float32)
+    goff = np.asarray(group_off, dtype=np.int64)
+    Q = len(goff) - 1
+    N = int(goff[-1])
+    keep = np.zeros(N, dtype=np.uint8)
+    counts = np.zeros(Q, dtype=np.int32)
+    for q in range(Q):
+        a, b = int(goff[q]), int(goff[q + 1])
+        toks = [tok[toff[i]:toff[i + 1]] for i in range(a, b)]
+        k, c = prune_prompt(toks, [float(x) for x in r32[a:b]],
+                            [int(x) for x in class_id[a:b]], ngram_n, tau_num, tau_den,
+                            keep_ratio, bool(group_valid[q]))
+        keep[a:b] = np.asarray(k, dtype=np.uint8)
+        counts[q] = c
+    return keep, counts
+
+
+def compact(keep_mask, traj_tok_off):
+    """Stream compaction of kept trajectories (ascending index).
+
+    Returns (kept_traj int32[Nk], kept_tok_off int64[Nk+1], tok_src int64[Tk]):
+    kept token t of the compacted stream comes from source token tok_src[t].
+    """
+    keep = np.asarray(keep_mask).astype(bool)
+    toff = np.asarray(traj_tok_off, dtype=np.int64)
+    kept = [i for i in range(len(keep)) if keep[i]]
+    off = [0]
+    src = []
+    for i in kept:
+        a, b = int(toff[i]), int(toff[i + 1])
+        src.extend(range(a, b))
+        off.append(off[-1] + (b - a))
+    return (np.asarray(kept, dtype=np.int32), np.asarray(off, dtype=np.int64),
+            np.asarray(src, dtype=np.int64))
