@@ -10,6 +10,7 @@ Readings where the paper is silent:
   equal float32 reward value: within a question A is a strictly increasing function
   of r whenever std > 0, and when std = 0 every A is 0 (one class).  Class ids are
   numbered 0, 1, ... in order of first occurrence inside the question.
+* a zero denominator (all rewards equal and eps = 0) gives A = 0.
 * DAPO-style dropping (``drop_uniform``): a question whose rewards are all equal
   is marked invalid (group_valid = 0).
 """
@@ -43,8 +44,10 @@ def group_advantage(rewards, group_off, ddof=1, eps=1e-6, drop_uniform=False):
             s = math.sqrt(sum((x - m) ** 2 for x in r) / (G - ddof))
         else:
             s = 0.0
+        den = s + eps
         for i, x in enumerate(r):
-            adv[a + i] = (x - m) / (s + eps)
+            # den == 0 only for an all-equal group with eps == 0: A = 0 (numerator is 0)
+            adv[a + i] = (x - m) / den if den > 0 else 0.0
         # classes: equal reward value, numbered by first occurrence
         seen = []
         for i, x in enumerate(r):

@@ -1,0 +1,948 @@
+// LM-head forward (logits + vocab-chunked online log-sum-exp + sampled-token gather),
+// the GRPO/DAPO/GSPO loss coefficient, and the LM-head backward, for gfx950.
+//
+// Sec. 3.2 (post-pruning evaluation) and Sec. 3.1 (Eq. 1, Eq. grad).  With P the softmax
+// of z = H W^T and g = dL/dlogp:  dZ = g (onehot(y) - P),  dH = dZ W,  dW = dZ^T H.
+//
+// One tiled GEMM kernel does the three contractions.  C[m, n] = sum_k A[m, k] B[n, k]
+// with both operands K-contiguous ("NT"), 256 x 256 block tiles, 4 wavefronts of
+// 128 x 128, LDS double buffering, and 32 x 32 MFMA tiles:
+//   bf16: v_mfma_f32_32x32x16_bf16, 64-wide K steps;  f32: v_mfma_f32_32x32x2_f32.
+// Both engines leave the accumulators in the same register layout, so the epilogues are
+// shared.  Work is cut into slabs of whole sequences; per slab:
+//   FWD  C = W . H_slab^T  (rows = vocab, cols = tokens, K = d).  Epilogue: per token,
+//        the block's max and sum exp(z - max) over its 256 vocab rows (in-lane over 64
+//        values, then one lane swap and one LDS exchange), the sampled token's logit,
+//        and E = exp(z - s_t) stored twice: E1[t][v] and E2[v][t].
+//   merge   partials -> lse, logp, row max; rows whose exp(z) would leave float range get
+//           s_t = max_t and their token block is evaluated again (rare).
+//   loss    g_t and c_t = g_t exp(s_t - lse_t) per token (one block per sequence).
+//   DH   C = E1 . W^T  (rows = tokens, cols = d, K = vocab):
+//        dH[t] = g_t W[y_t] - c_t C[t].
+//   DW   C = E2 . Bd^T with Bd[n][t] = c_t H[t][n]  (rows = vocab, cols = d, K = tokens):
+//        dW[v] (+)= -C[v] + sum_{t in slab, y_t = v} g_t H[t].
+// Nothing of size [T, V] exists; the slab buffers hold [slab, V].
+#include <algorithm>
+#include <vector>
+
+#include "common.h"
+
+namespace fastrl {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kBM = 256, kBN = 256, kThreads = 256;
+
+template <typename T>
+struct Eng;
+
+template <>
+struct Eng<uint16_t> {     // bfloat16 operands
+  static constexpr int BK = 64;
+  static constexpr int KP = 8;             // row padding (elements) against bank conflicts
+  static constexpr int LD = BK + KP;       // LDS row stride in elements
+  static constexpr int VEC = 8;            // elements per 16-byte vector
+  static constexpr int KSTEP = 16;         // K per MFMA
+};
+template <>
+struct Eng<float> {        // float32 operands
+  static constexpr int BK = 16;
+  static constexpr int KP = 4;
+  static constexpr int LD = BK + KP;
+  static constexpr int VEC = 4;
+  static constexpr int KSTEP = 2;
+};
+
+enum GemmMode { MODE_FWD = 0, MODE_DH = 1, MODE_DW = 2 };
+
+struct GemmParams {
+  const void* A;            // [M, lda]
+  int64_t lda;
+  int32_t M;
+  const void* B;            // [N rows, ldb] (rows via b_rows when non-null)
+  int64_t ldb;
+  int32_t N;
+  const int32_t* b_rows;    // FWD: row_index (nullable) offset to the slab
+  int64_t b_row_base;       // FWD: first kept token of the slab
+  int32_t K;
+  int32_t nmb, nnb;         // block grid (M blocks, N blocks)
+  // ---- FWD epilogue
+  float* pmax;              // [nmb][ldp]
+  float* psum;              // [nmb][ldp]
+  int64_t ldp;
+  float* zlab;              // [slab]
+  const int32_t* yslab;     // [slab] label of each slab token (-1: invalid)
+  const float* shift;       // [slab] s_t (nullable = 0)
+  void* E1;                 // [ldE1 rows][V_pad]   E1[t][v]
+  void* E2;                 // [V_pad][Tc_pad]     E2[v][t]
+  int64_t ldE1, ldE2;
+  int32_t Vreal;
+  int32_t store_e;          // 0: partials only, 1: partials + E, 2: E only (redo pass)
+  const int32_t* redo_blk;  // [nnb] token blocks to evaluate again (store_e == 2)
+  // ---- DH epilogue
+  void* dH;                 // [.., d] at slab offset
+  int32_t dH_bf16;
+  const float* gslab;       // [slab]
+  const float* cslab;       // [slab]
+  const void* W;            // [V, d]   (labels' rows)
+  int32_t d;
+  // ---- DW epilogue
+  float* dW;                // [V, d]
+  int32_t dW_acc;
+  const int32_t* lab_off;   // [V+1]  slab tokens grouped by label
+  const int32_t* lab_tok;   // [slab]
+  const void* H;            // hidden
+  const int32_t* row_index; // nullable
+  int64_t row_base;         // first kept token of the slab
+  int32_t* status;
+};
+
+__device__ __forceinline__ void tile_coords(int& mb, int& nb, int nmb, int nnb) {
+  const int nblk = gridDim.x;
+  int b = blockIdx.x;
+  // consecutive logical tiles on the same XCD (blocks are dealt round-robin to 8 XCDs)
+  const int full = (nblk / 8) * 8;
+  if (b < full) b = (b % 8) * (full / 8) + b / 8;
+  // grouped order: 8 M-blocks share each N-block sweep
+  constexpr int GROUP = 8;
+  const int per_group = GROUP * nnb;
+  const int gid = b / per_group;
+  const int first = gid * GROUP;
+  const int gsz = min(nmb - first, GROUP);
+  const int in = b % per_group;
+  mb = first + in % gsz;
+  nb = in / gsz;
+}
+
+template <typename T>
+__device__ __forceinline__ void load_vec(const T* p, bool ok, u32x4_t& v) {
+  if (ok) v = *reinterpret_cast<const u32x4_t*>(p);
+  else v = u32x4_t{0u, 0u, 0u, 0u};
+}
+
+template <typename T>
+__device__ __forceinline__ float to_f32(T x);
+template <>
+__device__ __forceinline__ float to_f32<uint16_t>(uint16_t x) { return bf16_to_f32(x); }
+template <>
+__device__ __forceinline__ float to_f32<float>(float x) { return x; }
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ uint16_t from_f32<uint16_t>(float x) { return f32_to_bf16(x); }
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+
+// accumulator (mi, ni, r) -> (row, col) inside the 256 x 256 block tile
+__device__ __forceinline__ int acc_row(int wm, int mi, int r, int lane) {
+  return wm * 128 + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+}
+__device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
+  return wn * 128 + ni * 32 + (lane & 31);
+}
+
+template <typename T, int MODE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void lm_gemm_kernel(const GemmParams p) {
+  using E = Eng<T>;
+  constexpr int BK = E::BK, LD = E::LD, VEC = E::VEC;
+  constexpr int VPR = BK / VEC;                       // vectors per tile row
+  constexpr int LOADS = kBM * VPR / kThreads;         // vectors per thread per operand
+  __shared__ __attribute__((aligned(16))) T smem[2 * 2 * kBM * LD];
+  T* As = smem;
+  T* Bs = smem + 2 * kBM * LD;
+
+  int mb, nb;
+  tile_coords(mb, nb, p.nmb, p.nnb);
+  if (MODE == MODE_FWD && p.store_e == 2 && p.redo_blk[nb] == 0) return;
+  const int m0 = mb * kBM, n0 = nb * kBN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  const T* Ag = static_cast<const T*>(p.A);
+  const T* Bg = static_cast<const T*>(p.B);
+  // per-thread global source rows (fixed for the whole K loop)
+  const T* arow[LOADS];
+  const T* brow[LOADS];
+  bool aok[LOADS], bok[LOADS];
+  int kofs[LOADS], srow[LOADS];
+#pragma unroll
+  for (int j = 0; j < LOADS; ++j) {
+    const int v = tid + j * kThreads;
+    const int row = v / VPR;
+    kofs[j] = (v % VPR) * VEC;
+    srow[j] = row;
+    const int am = m0 + row;
+    aok[j] = am < p.M;
+    arow[j] = Ag + int64_t(aok[j] ? am : 0) * p.lda;
+    const int bn = n0 + row;
+    bok[j] = bn < p.N;
+    int64_t br = bok[j] ? bn : 0;
+    if (MODE == MODE_FWD) {
+      br += p.b_row_base;
+      if (p.b_rows) br = bok[j] ? p.b_rows[br] : 0;
+    }
+    brow[j] = Bg + br * p.ldb;
+  }
+
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
+
+  u32x4_t ra[LOADS], rb[LOADS];
+  const int nk = (p.K + BK - 1) / BK;
+  auto gload = [&](int kt) {
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      const int k = k0 + kofs[j];
+      load_vec<T>(arow[j] + k, aok[j] && k < p.K, ra[j]);
+      load_vec<T>(brow[j] + k, bok[j] && k < p.K, rb[j]);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      *reinterpret_cast<u32x4_t*>(As + (buf * kBM + srow[j]) * LD + kofs[j]) = ra[j];
+      *reinterpret_cast<u32x4_t*>(Bs + (buf * kBM + srow[j]) * LD + kofs[j]) = rb[j];
+    }
+  };
+
+  gload(0);
+  sstore(0);
+  for (int kt = 0; kt < nk; ++kt) {
+    __syncthreads();
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload(kt + 1);
+    const T* as = As + buf * kBM * LD;
+    const T* bs = Bs + buf * kBM * LD;
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int kk = 0; kk < BK; kk += 16) {
+        bf16x8_t af[4], bf[4];
+        const int kq = kk + (lane >> 5) * 8;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          af[i] = *reinterpret_cast<const bf16x8_t*>(
+              as + (wm * 128 + i * 32 + (lane & 31)) * LD + kq);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          bf[j] = *reinterpret_cast<const bf16x8_t*>(
+              bs + (wn * 128 + j * 32 + (lane & 31)) * LD + kq);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < BK; kk += 2) {
+        float af[4], bf[4];
+        const int kq = kk + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af[i] = as[(wm * 128 + i * 32 + (lane & 31)) * LD + kq];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bf[j] = bs[(wn * 128 + j * 32 + (lane & 31)) * LD + kq];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
+    }
+    if (kt + 1 < nk) sstore(buf ^ 1);
+  }
+
+  // ------------------------------------------------------------------ epilogues
+  if constexpr (MODE == MODE_FWD) {
+    __syncthreads();  // LDS operand buffers are reused for the cross-wave exchange
+    float* xmax = reinterpret_cast<float*>(smem);      // [2 wm][256 cols]
+    float* xsum = xmax + 2 * kBN;
+    const int Vr = p.Vreal;
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) {
+      const int cl = acc_col(wn, ni, lane);
+      const int t = n0 + cl;                 // slab token
+      const bool tok_ok = t < p.N;
+      const int y = tok_ok ? p.yslab[t] : -1;
+      const float s_t = (tok_ok && p.shift) ? p.shift[t] : 0.0f;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = m0 + acc_row(wm, mi, r, lane);
+          const float z = acc[mi][ni][r];
+          if (v < Vr) mx = fmaxf(mx, z);
+          if (v == y && p.store_e != 2) p.zlab[t] = z;
+        }
+      if (p.store_e != 2) {
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        if (lane < 32) xmax[wm * kBN + cl] = mx;
+      }
+      if (p.store_e) {
+        // E = exp(z - s_t), zero outside [0, V) x [0, N)
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            T e4[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int r = rg * 4 + q;
+              const int v = m0 + acc_row(wm, mi, r, lane);
+              const float e = (tok_ok && v < Vr) ? __expf(acc[mi][ni][r] - s_t) : 0.0f;
+              e4[q] = from_f32<T>(e);
+            }
+            const int v0 = m0 + acc_row(wm, mi, rg * 4, lane);
+            T* e1 = static_cast<T*>(p.E1) + int64_t(t) * p.ldE1 + v0;
+            if constexpr (sizeof(T) == 2) {
+              uint2 pk;
+              pk.x = uint32_t(e4[0]) | (uint32_t(e4[1]) << 16);
+              pk.y = uint32_t(e4[2]) | (uint32_t(e4[3]) << 16);
+              *reinterpret_cast<uint2*>(e1) = pk;
+            } else {
+              *reinterpret_cast<float4*>(e1) = make_float4(e4[0], e4[1], e4[2], e4[3]);
+            }
+            if (p.E2) {
+              T* e2 = static_cast<T*>(p.E2) + int64_t(v0) * p.ldE2 + t;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) e2[int64_t(q) * p.ldE2] = e4[q];
+            }
+          }
+      }
+    }
+    if (p.store_e == 2) return;
+    __syncthreads();
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) {
+      const int cl = acc_col(wn, ni, lane);
+      const float M = fmaxf(xmax[cl], xmax[kBN + cl]);
+      float s = 0.0f;
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = m0 + acc_row(wm, mi, r, lane);
+          if (v < Vr) s += __expf(acc[mi][ni][r] - M);
+        }
+      s += __shfl_xor(s, 32, 64);
+      if (lane < 32) xsum[wm * kBN + cl] = s;
+    }
+    __syncthreads();
+    for (int cl = tid; cl < kBN; cl += kThreads) {
+      const int t = n0 + cl;
+      if (t < p.N) {
+        p.pmax[int64_t(mb) * p.ldp + t] = fmaxf(xmax[cl], xmax[kBN + cl]);
+        p.psum[int64_t(mb) * p.ldp + t] = xsum[cl] + xsum[kBN + cl];
+      }
+    }
+  } else if constexpr (MODE == MODE_DH) {
+    const T* Wg = static_cast<const T*>(p.W);
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int t = m0 + acc_row(wm, mi, r, lane);
+        if (t < p.M) {
+          const int y = p.yslab[t];
+          const float g = p.gslab[t], c = p.cslab[t];
+#pragma unroll
+          for (int ni = 0; ni < 4; ++ni) {
+            const int n = n0 + acc_col(wn, ni, lane);
+            if (n < p.N) {
+              const float wy = y >= 0 ? to_f32<T>(Wg[int64_t(y) * p.d + n]) : 0.0f;
+              const float val = g * wy - c * acc[mi][ni][r];
+              const int64_t o = int64_t(t) * p.d + n;
+              if (p.dH_bf16) static_cast<uint16_t*>(p.dH)[o] = f32_to_bf16(val);
+              else static_cast<float*>(p.dH)[o] = val;
+            }
+          }
+        }
+      }
+  } else {  // MODE_DW
+    const T* Hg = static_cast<const T*>(p.H);
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = m0 + acc_row(wm, mi, r, lane);
+        if (v < p.M) {
+          // onehot part: sum of g_t H[t] over the slab tokens labelled v (index order)
+          float oh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+          const int b0 = p.lab_off[v], b1 = p.lab_off[v + 1];
+          for (int e = b0; e < b1; ++e) {
+            const int t = p.lab_tok[e];
+            int64_t row = p.row_base + t;
+            if (p.row_index) row = p.row_index[row];
+            const float gt = p.gslab[t];
+            const T* hrow = Hg + row * p.d;
+#pragma unroll
+            for (int ni = 0; ni < 4; ++ni) {
+              const int n = n0 + acc_col(wn, ni, lane);
+              oh[ni] += n < p.N ? gt * to_f32<T>(hrow[n]) : 0.0f;
+            }
+          }
+#pragma unroll
+          for (int ni = 0; ni < 4; ++ni) {
+            const int n = n0 + acc_col(wn, ni, lane);
+            if (n < p.N) {
+              const int64_t o = int64_t(v) * p.d + n;
+              const float prev = p.dW_acc ? p.dW[o] : 0.0f;
+              p.dW[o] = prev + oh[ni] - acc[mi][ni][r];
+            }
+          }
+        }
+      }
+  }
+}
+
+// ------------------------------------------------------------------ small kernels
+
+// s_t = 0, labels of the slab, validity
+__global__ void slab_prep_kernel(const int32_t* __restrict__ token_ids,
+                                 const int32_t* __restrict__ row_index, int64_t row_base,
+                                 int32_t Tc, int32_t V, int32_t* __restrict__ yslab,
+                                 float* __restrict__ shift, int32_t* __restrict__ status) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Tc) return;
+  int64_t row = row_base + t;
+  if (row_index) row = row_index[row];
+  int y = token_ids[row];
+  if (y < 0 || y >= V) {
+    set_status(status, FASTRL_SB_BAD_TOKEN);
+    y = -1;
+  }
+  yslab[t] = y;
+  if (shift) shift[t] = 0.0f;
+}
+
+// partials -> lse, logp; decide whether a row needs a shifted second pass
+__global__ void merge_kernel(const float* __restrict__ pmax, const float* __restrict__ psum,
+                             int64_t ldp, int32_t nmb, const float* __restrict__ zlab,
+                             const int32_t* __restrict__ yslab, int32_t Tc,
+                             float* __restrict__ lse_out, float* __restrict__ logp_out,
+                             float* __restrict__ shift, int32_t* __restrict__ redo_blk,
+                             int32_t* __restrict__ redo_count) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= Tc) return;
+  float M = -INFINITY;
+  for (int b = 0; b < nmb; ++b) M = fmaxf(M, pmax[int64_t(b) * ldp + t]);
+  float S = 0.0f;
+  for (int b = 0; b < nmb; ++b) S += psum[int64_t(b) * ldp + t] * __expf(pmax[int64_t(b) * ldp + t] - M);
+  const float l = M + __logf(S);
+  const int y = yslab[t];
+  if (lse_out) lse_out[t] = l;
+  if (logp_out) logp_out[t] = y >= 0 ? zlab[t] - l : __int_as_float(0x7fc00000);
+  if (shift) {
+    // E = exp(z - s) must stay finite (z - s <= max - s < 80) and the dominant entries
+    // normal (max - s > -60); s = 0 fails only for extreme logits
+    if (!(M < 80.0f && M > -60.0f)) {
+      shift[t] = M;
+      redo_blk[t / kBN] = 1;
+      atomicAdd(redo_count, 1);
+    }
+  }
+}
+
+__device__ __forceinline__ double block_sum_d(double v, double* red) {
+  // fixed-shape tree: wave butterfly, then the 4 wave sums in order
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wv] = v;
+  __syncthreads();
+  double s = 0.0;
+  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) s += red[w];
+  return s;
+}
+
+// one block per sequence of the slab: g_t, c_t and the sequence's loss term
+__global__ __launch_bounds__(256) void loss_kernel(
+    const float* __restrict__ logp, const float* __restrict__ lse,
+    const float* __restrict__ old_logp, const float* __restrict__ ref_logp,
+    const int32_t* __restrict__ row_index, const int64_t* __restrict__ seq_off,
+    const float* __restrict__ adv, const int32_t* __restrict__ seq_index, int32_t S,
+    int64_t T, int32_t seq_begin, int64_t row_base, int32_t algo, int32_t norm,
+    float eps_low, float eps_high, float beta, const float* __restrict__ shift,
+    float* __restrict__ gslab, float* __restrict__ cslab, double* __restrict__ seq_loss,
+    int32_t* __restrict__ seq_clip, int32_t* __restrict__ status, int32_t nadv) {
+  __shared__ double red[4];
+  __shared__ double redc[4];
+  const int i = seq_begin + blockIdx.x;
+  const int64_t a = seq_off[i], b = seq_off[i + 1];
+  const int64_t L = b - a;
+  int ai = seq_index ? seq_index[i] : i;
+  if (ai < 0 || ai >= nadv) {
+    if (threadIdx.x == 0) set_status(status, FASTRL_SB_BAD_INDEX);
+    ai = -1;
+  }
+  const double A = ai >= 0 ? double(adv[ai]) : 0.0;
+  const double w = (norm == FASTRL_NORM_TOKEN_MEAN) ? 1.0 / double(T)
+                                                    : (L > 0 ? 1.0 / (double(S) * double(L)) : 0.0);
+  const double lo = 1.0 - double(eps_low), hi = 1.0 + double(eps_high);
+  const bool kl = beta != 0.0f;
+  double part = 0.0;  // this sequence's contribution to the loss
+  int clip = 0;
+  double sratio = 0.0, cseq = 0.0;
+  if (algo == FASTRL_GSPO && L > 0) {
+    double sl = 0.0;
+    for (int64_t t = a + threadIdx.x; t < b; t += blockDim.x) {
+      int64_t row = t;
+      if (row_index) row = row_index[t];
+      sl += double(logp[t]) - double(old_logp[row]);
+    }
+    sl = block_sum_d(sl, red);
+    sratio = exp(sl / double(L));
+    const double sur = fmin(sratio * A, fmin(fmax(sratio, lo), hi) * A);
+    cseq = ((A >= 0.0 && sratio <= hi) || (A < 0.0 && sratio >= lo)) ? 1.0 : 0.0;
+    if (threadIdx.x == 0) part = -(w * double(L)) * sur;
+    clip = (cseq == 0.0) ? int(L) : 0;
+  }
+  double kpart = 0.0;
+  for (int64_t t = a + threadIdx.x; t < b; t += blockDim.x) {
+    int64_t row = t;
+    if (row_index) row = row_index[t];
+    const double x = logp[t];
+    double g;
+    if (algo == FASTRL_GSPO) {
+      g = (w * double(L)) * (-cseq * sratio * A / double(L));
+    } else {
+      const double rho = exp(x - double(old_logp[row]));
+      const double sur = fmin(rho * A, fmin(fmax(rho, lo), hi) * A);
+      const double c = ((A >= 0.0 && rho <= hi) || (A < 0.0 && rho >= lo)) ? 1.0 : 0.0;
+      kpart += -w * sur;
+      g = w * (-c * rho * A);
+      clip += (c == 0.0);
+    }
+    if (kl) {
+      const double f = ref_logp[row];
+      const double e = exp(f - x);
+      kpart += double(beta) * w * (e - (f - x) - 1.0);
+      g += double(beta) * w * (1.0 - e);
+    }
+    const int64_t tl = t - row_base;
+    gslab[tl] = float(g);
+    const float s_t = shift ? shift[tl] : 0.0f;
+    cslab[tl] = float(g * exp(double(s_t) - double(lse[t])));
+  }
+  kpart = block_sum_d(kpart, red);
+  const double clips = block_sum_d(algo == FASTRL_GSPO ? 0.0 : double(clip), redc);
+  if (threadIdx.x == 0) {
+    seq_loss[i] = part + kpart;
+    seq_clip[i] = algo == FASTRL_GSPO ? clip : int(clips);
+  }
+}
+
+// sum of per-sequence loss terms in index order (deterministic)
+__global__ void loss_final_kernel(const double* __restrict__ seq_loss,
+                                  const int32_t* __restrict__ seq_clip, int32_t S,
+                                  const int32_t* __restrict__ redo_count,
+                                  float* __restrict__ loss, float* __restrict__ stats) {
+  __shared__ double red[4];
+  __shared__ double redc[4];
+  double s = 0.0, c = 0.0;
+  // contiguous chunk per thread keeps the order fixed for a given S
+  const int per = (S + blockDim.x - 1) / blockDim.x;
+  const int b = threadIdx.x * per, e = min(S, b + per);
+  for (int i = b; i < e; ++i) {
+    s += seq_loss[i];
+    c += seq_clip[i];
+  }
+  s = block_sum_d(s, red);
+  c = block_sum_d(c, redc);
+  if (threadIdx.x == 0) {
+    loss[0] = float(s);
+    if (stats) {
+      stats[0] = float(c);
+      stats[1] = float(redo_count[0]);
+    }
+  }
+}
+
+// out[c][r] = scale(r) * in[row(r)][c], zero for r in [R, Rpad): tiled transpose via LDS
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_scale_kernel(
+    const T* __restrict__ in, const int32_t* __restrict__ row_index, int64_t row_base,
+    int32_t R, int32_t Rpad, int32_t C, const float* __restrict__ scale, T* __restrict__ out,
+    int64_t ldo) {
+  __shared__ float tile[64][65];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int rr = ty; rr < 64; rr += 4) {
+    const int r = r0 + rr;
+    float v = 0.0f;
+    if (r < R && c0 + tx < C) {
+      int64_t row = row_base + r;
+      if (row_index) row = row_index[row];
+      v = to_f32<T>(in[row * C + c0 + tx]);
+      if (scale) v *= scale[r];
+    }
+    tile[rr][tx] = v;
+  }
+  __syncthreads();
+  for (int cc = ty; cc < 64; cc += 4) {
+    const int c = c0 + cc;
+    const int r = r0 + tx;
+    if (c < C && r < Rpad) out[int64_t(c) * ldo + r] = from_f32<T>(tile[tx][cc]);
+  }
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+__global__ void label_hist_kernel(const int32_t* __restrict__ yslab, int32_t Tc,
+                                  int32_t* __restrict__ cnt) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < Tc && yslab[t] >= 0) atomicAdd(&cnt[yslab[t]], 1);
+}
+
+// exclusive scan of cnt[0..n) into off[0..n], cursor = copy of off
+__global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ cnt, int32_t n,
+                                                    int32_t* __restrict__ off,
+                                                    int32_t* __restrict__ cursor) {
+  __shared__ int32_t ws[16];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int32_t base = 0;
+  for (int c = 0; c < n; c += 1024) {
+    const int i = c + tid;
+    const int x = i < n ? cnt[i] : 0;
+    int v = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      int t = __shfl_up(v, o, 64);
+      if (lane >= o) v += t;
+    }
+    if (lane == 63) ws[wv] = v;
+    __syncthreads();
+    int pre = 0, tot = 0;
+    for (int w = 0; w < 16; ++w) {
+      if (w < wv) pre += ws[w];
+      tot += ws[w];
+    }
+    if (i < n) {
+      off[i] = base + pre + v - x;
+      cursor[i] = base + pre + v - x;
+    }
+    base += tot;
+    __syncthreads();
+  }
+  if (tid == 0) off[n] = base;
+}
+
+__global__ void label_fill_kernel(const int32_t* __restrict__ yslab, int32_t Tc,
+                                  int32_t* __restrict__ cursor, int32_t* __restrict__ lab_tok) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < Tc && yslab[t] >= 0) lab_tok[atomicAdd(&cursor[yslab[t]], 1)] = t;
+}
+
+// order each label bucket by token index so dW sums in a fixed order
+__global__ void label_sort_kernel(const int32_t* __restrict__ off, int32_t V,
+                                  int32_t* __restrict__ lab_tok) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= V) return;
+  const int a = off[v], b = off[v + 1];
+  for (int i = a + 1; i < b; ++i) {
+    const int x = lab_tok[i];
+    int j = i - 1;
+    while (j >= a && lab_tok[j] > x) {
+      lab_tok[j + 1] = lab_tok[j];
+      --j;
+    }
+    lab_tok[j + 1] = x;
+  }
+}
+
+// ------------------------------------------------------------------ host side
+
+static inline int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+template <typename T, int MODE>
+static int launch_gemm(GemmParams p, int kind, double flops, hipStream_t stream) {
+  p.nmb = int((p.M + kBM - 1) / kBM);
+  p.nnb = int((p.N + kBN - 1) / kBN);
+  const int64_t nblk = int64_t(p.nmb) * p.nnb;
+  if (nblk == 0) return FASTRL_OK;
+  ProfScope prof(kind, stream, flops);
+  hipLaunchKernelGGL((lm_gemm_kernel<T, MODE>), dim3(unsigned(nblk)), dim3(kThreads), 0,
+                     stream, p);
+  FR_LAUNCHED();
+  return FASTRL_OK;
+}
+
+#define FR_TRY(x)                 \
+  do {                            \
+    int rc_ = (x);                \
+    if (rc_ != FASTRL_OK) return rc_; \
+  } while (0)
+
+static inline unsigned nb1d(int64_t n, int b) { return unsigned((n + b - 1) / b); }
+
+// ---------------------------------------------------------------- token log-prob only
+constexpr int64_t kLogprobChunk = 65536;
+
+struct LogprobWs {
+  float *pmax, *psum, *zlab;
+  int32_t* yslab;
+};
+
+static size_t carve_logprob(Carver& c, LogprobWs& w, int64_t T, int32_t V) {
+  const int64_t ch = rup(std::min<int64_t>(std::max<int64_t>(T, 1), kLogprobChunk), 256);
+  const int64_t nmb = (V + kBM - 1) / kBM;
+  w.pmax = c.take<float>(size_t(nmb * ch));
+  w.psum = c.take<float>(size_t(nmb * ch));
+  w.zlab = c.take<float>(size_t(ch));
+  w.yslab = c.take<int32_t>(size_t(ch));
+  return c.size();
+}
+
+size_t token_logprob_workspace(int64_t T, int32_t d, int32_t V, int32_t dtype) {
+  (void)d;
+  (void)dtype;
+  Carver c(nullptr);
+  LogprobWs w;
+  return carve_logprob(c, w, T, V);
+}
+
+template <typename T>
+static int token_logprob_impl(const void* hidden, const int32_t* row_index, const void* W,
+                              int64_t Tn, int32_t d, int32_t V, const int32_t* token_ids,
+                              float* logp, float* lse, int32_t* status, void* ws,
+                              hipStream_t stream) {
+  Carver c(ws);
+  LogprobWs w;
+  carve_logprob(c, w, Tn, V);
+  const int64_t ch = rup(std::min<int64_t>(std::max<int64_t>(Tn, 1), kLogprobChunk), 256);
+  for (int64_t t0 = 0; t0 < Tn; t0 += kLogprobChunk) {
+    const int32_t Tc = int32_t(std::min<int64_t>(kLogprobChunk, Tn - t0));
+    hipLaunchKernelGGL(slab_prep_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream, token_ids,
+                       row_index, t0, Tc, V, w.yslab, (float*)nullptr, status);
+    FR_LAUNCHED();
+    GemmParams p{};
+    p.A = W; p.lda = d; p.M = V;
+    p.B = hidden; p.ldb = d; p.N = Tc; p.b_rows = row_index; p.b_row_base = t0;
+    p.K = d;
+    p.pmax = w.pmax; p.psum = w.psum; p.ldp = ch; p.zlab = w.zlab; p.yslab = w.yslab;
+    p.Vreal = V; p.store_e = 0; p.status = status;
+    FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, 2.0 * V * double(Tc) * d, stream)));
+    const int32_t nmb = (V + kBM - 1) / kBM;
+    hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream, w.pmax, w.psum,
+                       ch, nmb, w.zlab, w.yslab, Tc, lse ? lse + t0 : (float*)nullptr,
+                       logp + t0, (float*)nullptr, (int32_t*)nullptr, (int32_t*)nullptr);
+    FR_LAUNCHED();
+  }
+  return FASTRL_OK;
+}
+
+int run_token_logprob(const void* hidden, const int32_t* row_index, const void* W,
+                      int32_t dtype, int64_t T, int32_t d, int32_t V,
+                      const int32_t* token_ids, float* logp, float* lse, int32_t* status,
+                      void* ws, hipStream_t stream) {
+  if (dtype == FASTRL_BF16)
+    return token_logprob_impl<uint16_t>(hidden, row_index, W, T, d, V, token_ids, logp, lse,
+                                        status, ws, stream);
+  return token_logprob_impl<float>(hidden, row_index, W, T, d, V, token_ids, logp, lse, status,
+                                   ws, stream);
+}
+
+// ---------------------------------------------------------------- loss forward/backward
+constexpr int64_t kDefaultSlab = 16384;
+
+struct SlabPlan {
+  std::vector<int32_t> seq_begin;  // first sequence of each slab; back() == S
+  int64_t tc_max = 0;
+};
+
+static SlabPlan plan_slabs(const int64_t* off, int32_t S, int64_t cap) {
+  SlabPlan pl;
+  int32_t i = 0;
+  while (i < S) {
+    pl.seq_begin.push_back(i);
+    const int64_t start = off[i];
+    int32_t j = i + 1;
+    while (j < S && off[j + 1] - start <= cap) ++j;
+    pl.tc_max = std::max<int64_t>(pl.tc_max, off[j] - start);
+    i = j;
+  }
+  pl.seq_begin.push_back(S);
+  return pl;
+}
+
+struct LossWs {
+  void *WT, *E1, *E2, *Bd;
+  float *pmax, *psum, *zlab, *shift, *gslab, *cslab, *lse, *logp;
+  int32_t *yslab, *redo_blk, *redo_count, *seq_clip, *lab_cnt, *lab_off, *lab_cur, *lab_tok;
+  double* seq_loss;
+};
+
+static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_t tc_max) {
+  const int esz = a.dtype == FASTRL_BF16 ? 2 : 4;
+  const int64_t Vpad = rup(a.V, kBM);
+  const int64_t tcp = rup(std::max<int64_t>(tc_max, 1), kBN);
+  const int64_t nmb = Vpad / kBM;
+  const bool dh = a.dhidden != nullptr, dw = a.dW != nullptr;
+  w.WT = dh ? c.take<char>(size_t(a.d) * Vpad * esz) : nullptr;
+  w.E1 = (dh || dw) ? c.take<char>(size_t(tcp) * Vpad * esz) : nullptr;
+  w.E2 = dw ? c.take<char>(size_t(Vpad) * tcp * esz) : nullptr;
+  w.Bd = dw ? c.take<char>(size_t(a.d) * tcp * esz) : nullptr;
+  w.pmax = c.take<float>(size_t(nmb * tcp));
+  w.psum = c.take<float>(size_t(nmb * tcp));
+  w.zlab = c.take<float>(size_t(tcp));
+  w.shift = c.take<float>(size_t(tcp));
+  w.gslab = c.take<float>(size_t(tcp));
+  w.cslab = c.take<float>(size_t(tcp));
+  w.yslab = c.take<int32_t>(size_t(tcp));
+  w.redo_blk = c.take<int32_t>(size_t(tcp / kBN));
+  w.redo_count = c.take<int32_t>(1);
+  w.lse = a.lse ? a.lse : c.take<float>(size_t(std::max<int64_t>(a.T, 1)));
+  w.logp = a.logp ? a.logp : c.take<float>(size_t(std::max<int64_t>(a.T, 1)));
+  w.seq_loss = c.take<double>(size_t(std::max(a.S, 1)));
+  w.seq_clip = c.take<int32_t>(size_t(std::max(a.S, 1)));
+  w.lab_cnt = c.take<int32_t>(size_t(a.V + 1));
+  w.lab_off = c.take<int32_t>(size_t(a.V + 1));
+  w.lab_cur = c.take<int32_t>(size_t(a.V + 1));
+  w.lab_tok = c.take<int32_t>(size_t(tcp));
+  return c.size();
+}
+
+static int64_t slab_cap(const fastrl_loss_args& a) {
+  return a.slab_tokens > 0 ? a.slab_tokens : kDefaultSlab;
+}
+
+size_t policy_loss_workspace(const fastrl_loss_args& a) {
+  SlabPlan pl = plan_slabs(a.seq_off_host, a.S, slab_cap(a));
+  Carver c(nullptr);
+  LossWs w;
+  return carve_loss(c, w, a, pl.tc_max);
+}
+
+template <typename T>
+static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
+  SlabPlan pl = plan_slabs(a.seq_off_host, a.S, slab_cap(a));
+  Carver c(a.ws);
+  LossWs w;
+  carve_loss(c, w, a, pl.tc_max);
+  const int64_t Vpad = rup(a.V, kBM);
+  const int64_t tcp = rup(std::max<int64_t>(pl.tc_max, 1), kBN);
+  const int32_t nmb = int32_t(Vpad / kBM);
+  const bool dh = a.dhidden != nullptr, dw = a.dW != nullptr;
+  const int32_t d = a.d, V = a.V;
+
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, stream, w.redo_count, int64_t(1), 0);
+  FR_LAUNCHED();
+  if (dw && !a.dW_accumulate && a.S == 0) {
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(1024), dim3(256), 0, stream,
+                       reinterpret_cast<int32_t*>(a.dW), int64_t(V) * d, 0);
+    FR_LAUNCHED();
+  }
+  if (dh && a.S > 0) {
+    dim3 g(nb1d(d, 64), unsigned(Vpad / 64));
+    hipLaunchKernelGGL((transpose_scale_kernel<T>), g, dim3(256), 0, stream,
+                       static_cast<const T*>(a.W), (const int32_t*)nullptr, int64_t(0), V,
+                       int32_t(Vpad), d, (const float*)nullptr, static_cast<T*>(w.WT), Vpad);
+    FR_LAUNCHED();
+  }
+  const size_t nslab = pl.seq_begin.size() - 1;
+  for (size_t si = 0; si < nslab; ++si) {
+    const int32_t s0 = pl.seq_begin[si], s1 = pl.seq_begin[si + 1];
+    const int64_t t0 = a.seq_off_host[s0];
+    const int32_t Tc = int32_t(a.seq_off_host[s1] - t0);
+    const int64_t Tr = rup(std::max<int32_t>(Tc, 1), kBN);
+    const int32_t nnb = int32_t(Tr / kBN);
+    hipLaunchKernelGGL(slab_prep_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0, stream,
+                       a.token_ids, a.row_index, t0, Tc, V, w.yslab, w.shift, a.status);
+    FR_LAUNCHED();
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(256), 0, stream, w.redo_blk,
+                       int64_t(nnb), 0);
+    FR_LAUNCHED();
+    GemmParams p{};
+    p.A = a.W; p.lda = d; p.M = V;
+    p.B = a.hidden; p.ldb = d; p.N = Tc; p.b_rows = a.row_index; p.b_row_base = t0;
+    p.K = d;
+    p.pmax = w.pmax; p.psum = w.psum; p.ldp = tcp; p.zlab = w.zlab; p.yslab = w.yslab;
+    p.shift = w.shift; p.E1 = w.E1; p.E2 = w.E2; p.ldE1 = Vpad; p.ldE2 = tcp;
+    p.Vreal = V; p.store_e = (dh || dw) ? 1 : 0; p.status = a.status;
+    p.redo_blk = w.redo_blk;
+    const double f_fwd = 2.0 * double(V) * Tc * d;
+    FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, f_fwd, stream)));
+    hipLaunchKernelGGL(merge_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0, stream,
+                       w.pmax, w.psum, tcp, nmb, w.zlab, w.yslab, Tc, w.lse + t0, w.logp + t0,
+                       (dh || dw) ? w.shift : (float*)nullptr, w.redo_blk, w.redo_count);
+    FR_LAUNCHED();
+    if (dh || dw) {
+      p.store_e = 2;  // token blocks holding a shifted row: store E again
+      FR_TRY((launch_gemm<T, MODE_FWD>(p, -1, 0.0, stream)));
+    }
+    hipLaunchKernelGGL(loss_kernel, dim3(unsigned(s1 - s0)), dim3(256), 0, stream, w.logp,
+                       w.lse, a.old_logp, a.ref_logp, a.row_index, a.seq_off, a.adv,
+                       a.seq_index, a.S, a.T, s0, t0, a.algo, a.norm, a.eps_low, a.eps_high,
+                       a.beta, w.shift, w.gslab, w.cslab, w.seq_loss, w.seq_clip, a.status,
+                       a.seq_index ? INT32_MAX : a.S);
+    FR_LAUNCHED();
+    if (dh) {
+      GemmParams q{};
+      q.A = w.E1; q.lda = Vpad; q.M = Tc;
+      q.B = w.WT; q.ldb = Vpad; q.N = d;
+      q.K = int32_t(Vpad);
+      q.dH = a.dhidden_dtype == FASTRL_BF16
+                 ? (void*)(static_cast<uint16_t*>(a.dhidden) + t0 * d)
+                 : (void*)(static_cast<float*>(a.dhidden) + t0 * d);
+      q.dH_bf16 = a.dhidden_dtype == FASTRL_BF16;
+      q.gslab = w.gslab; q.cslab = w.cslab; q.yslab = w.yslab; q.W = a.W; q.d = d;
+      q.status = a.status;
+      FR_TRY((launch_gemm<T, MODE_DH>(q, FASTRL_K_DHIDDEN, 2.0 * double(Tc) * d * V, stream)));
+    }
+    if (dw) {
+      dim3 g(nb1d(d, 64), unsigned(Tr / 64));
+      hipLaunchKernelGGL((transpose_scale_kernel<T>), g, dim3(256), 0, stream,
+                         static_cast<const T*>(a.hidden), a.row_index, t0, Tc, int32_t(Tr), d,
+                         w.cslab, static_cast<T*>(w.Bd), tcp);
+      FR_LAUNCHED();
+      hipLaunchKernelGGL(fill_i32_kernel, dim3(256), dim3(256), 0, stream, w.lab_cnt,
+                         int64_t(V), 0);
+      FR_LAUNCHED();
+      hipLaunchKernelGGL(label_hist_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0,
+                         stream, w.yslab, Tc, w.lab_cnt);
+      FR_LAUNCHED();
+      hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, w.lab_cnt, V, w.lab_off,
+                         w.lab_cur);
+      FR_LAUNCHED();
+      hipLaunchKernelGGL(label_fill_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0,
+                         stream, w.yslab, Tc, w.lab_cur, w.lab_tok);
+      FR_LAUNCHED();
+      hipLaunchKernelGGL(label_sort_kernel, dim3(nb1d(V, 256)), dim3(256), 0, stream,
+                         w.lab_off, V, w.lab_tok);
+      FR_LAUNCHED();
+      GemmParams q{};
+      q.A = w.E2; q.lda = tcp; q.M = V;
+      q.B = w.Bd; q.ldb = tcp; q.N = d;
+      q.K = int32_t(Tr);
+      q.dW = a.dW; q.dW_acc = (si > 0 || a.dW_accumulate) ? 1 : 0;
+      q.lab_off = w.lab_off; q.lab_tok = w.lab_tok; q.gslab = w.gslab;
+      q.H = a.hidden; q.row_index = a.row_index; q.row_base = t0; q.d = d;
+      q.status = a.status;
+      FR_TRY((launch_gemm<T, MODE_DW>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
+    }
+  }
+  hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, stream, w.seq_loss, w.seq_clip,
+                     a.S, w.redo_count, a.loss, a.stats);
+  FR_LAUNCHED();
+  return FASTRL_OK;
+}
+
+int run_policy_loss(const fastrl_loss_args& a, hipStream_t stream) {
+  if (a.dtype == FASTRL_BF16) return policy_loss_impl<uint16_t>(a, stream);
+  return policy_loss_impl<float>(a, stream);
+}
+
+}  // namespace fastrl

@@ -172,3 +172,25 @@ def make_dense(cfg, T_rows, device="cpu", seed=None, d=None, V=None, chunk=1 << 
         return out
 
     return draw(T_rows, h_std, 7), draw(V, w_std, 8)
+
+
+def plant_duplicates(ro, p_copy=0.6, p_mutate=0.15, seed=7):
+    """Test-only structure: inside each question, overwrite some trajectories with a
+    near-copy of the question's first trajectory (each position re-drawn with probability
+    p_mutate), so n-gram Jaccard distances fall below tau and MDAP has work to do.
+    Modifies ``ro.token_ids`` in place."""
+    rng = _rng(seed, 99)
+    V = int(ro.extra["V"])
+    for q in range(len(ro.group_off) - 1):
+        a, b = int(ro.group_off[q]), int(ro.group_off[q + 1])
+        base = ro.token_ids[ro.traj_tok_off[a]:ro.traj_tok_off[a + 1]].copy()
+        for i in range(a + 1, b):
+            if rng.uniform() >= p_copy or len(base) == 0:
+                continue
+            s0, s1 = int(ro.traj_tok_off[i]), int(ro.traj_tok_off[i + 1])
+            L = s1 - s0
+            t = np.resize(base, L)
+            m = rng.uniform(size=L) < p_mutate
+            t[m] = rng.integers(0, V, size=int(m.sum()))
+            ro.token_ids[s0:s1] = t
+    return ro

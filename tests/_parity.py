@@ -1,0 +1,131 @@
+"""Shared helpers of the GPU parity tests: build one seeded problem, run the oracle and
+the HIP path (through the C ABI) on the same inputs, compare with the stated bars:
+pruning masks / indices bit-exact, log-probs 2e-3 absolute, loss and gradients 1e-2
+relative (bf16 inputs, fp32 accumulate)."""
+import dataclasses
+
+import numpy as np
+import torch
+
+import oracle
+from synth import CONFIGS, make_rollouts, make_dense, plant_duplicates
+
+LOGP_ATOL = 2e-3
+REL = 1e-2
+
+
+def rel_fro(a, b):
+    nb = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
+
+
+def to_dev(x, dev, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(dev)
+
+
+class Problem:
+    """Seeded problem: rollouts, oracle pruning, dense tensors and old/ref log-probs built
+    from the oracle's exact log-probs of the kept tokens (+ the seeded noise)."""
+
+    def __init__(self, cfg_id, dev, *, Q=None, len_range=None, G=None, V=None, d=None,
+                 dtype=None, seed=None, h_std=1.0, w_std=0.02, ngram_n=None, keep_ratio=None,
+                 tau=None, vocab_ids=None, planted=None):
+        base = CONFIGS[cfg_id]
+        self.cfg = base
+        self.V = V or base.V
+        self.d = d or base.d
+        self.dtype = dtype or base.dtype
+        self.keep_ratio = base.keep_ratio if keep_ratio is None else keep_ratio
+        self.tau = (base.tau_num, base.tau_den) if tau is None else tau
+        self.ngram_n = base.ngram_n if ngram_n is None else ngram_n
+        ro = make_rollouts(base, seed=seed, Q=Q, len_range=len_range, G=G, V=vocab_ids or self.V)
+        if planted is not None:
+            plant_duplicates(ro, **planted)
+        self.ro = ro
+        self.dev = dev
+        pr = oracle.hot_path_step(ro.rewards, ro.group_off, ro.token_ids, ro.traj_tok_off,
+                                  lmhead=False, ngram_n=self.ngram_n, tau_num=self.tau[0],
+                                  tau_den=self.tau[1], keep_ratio=self.keep_ratio,
+                                  drop_uniform=base.drop_uniform)
+        self.pr = pr
+        self.src = pr["tok_src"]
+        self.max_group = int(np.diff(ro.group_off).max())
+        self.max_len = int(ro.lengths.max())
+        cfg_dt = dataclasses.replace(base, dtype=self.dtype)
+        H, W = make_dense(cfg_dt, ro.T_total, device="cpu", d=self.d, V=self.V,
+                          seed=seed, h_std=h_std, w_std=w_std)
+        self.H, self.W = H, W
+        self.H64 = H.double().numpy()
+        self.W64 = W.double().numpy()
+        y = ro.token_ids[self.src].astype(np.int64)
+        self.y = y
+        lp, lse = oracle.token_logprob(self.H64[self.src], self.W64, y)
+        self.logp_exact, self.lse_exact = lp, lse
+        old = np.full(ro.T_total, np.nan)
+        ref = np.full(ro.T_total, np.nan)
+        old[self.src] = lp + ro.old_noise[self.src]
+        ref[self.src] = lp + ro.ref_noise[self.src]
+        self.old = old.astype(np.float32)
+        self.ref = ref.astype(np.float32)
+        # poison every pruned row: the HIP path must never read it
+        Hp = H.clone()
+        pruned = np.ones(ro.T_total, dtype=bool)
+        pruned[self.src] = False
+        Hp[torch.from_numpy(pruned)] = float("nan")
+        self.H_poisoned = Hp
+
+    def oracle_loss(self):
+        base = self.cfg
+        kept = self.pr["kept_traj"]
+        loss, g, info = oracle.policy_loss(
+            self.logp_exact, self.old[self.src].astype(np.float64),
+            self.ref[self.src].astype(np.float64) if base.beta else None,
+            self.pr["kept_tok_off"], self.pr["adv"][kept], algo=base.algo, norm=base.norm,
+            eps_low=base.eps_low, eps_high=base.eps_high, beta=base.beta)
+        dH, dW = oracle.lmhead_backward(self.H64[self.src], self.W64, self.y, self.lse_exact, g)
+        return dict(loss=loss, g=g, dH=dH, dW=dW, clipped=info["clipped_tokens"])
+
+    def run_gpu(self, fr, slab_tokens=0, dhidden_dtype=None, status=None, poisoned=True):
+        dev = self.dev
+        ro = self.ro
+        base = self.cfg
+        H = (self.H_poisoned if poisoned else self.H).to(dev)
+        W = self.W.to(dev)
+        old = to_dev(self.old, dev)
+        ref = to_dev(self.ref, dev) if base.beta else None
+        return fr.hot_path_step(
+            to_dev(ro.rewards, dev), to_dev(ro.group_off, dev), to_dev(ro.token_ids, dev),
+            to_dev(ro.traj_tok_off, dev), H, W, old, ref, V=self.V, max_group=self.max_group,
+            max_len=self.max_len, algo=base.algo, norm=base.norm, eps_low=base.eps_low,
+            eps_high=base.eps_high, beta=base.beta, ngram_n=self.ngram_n, tau=self.tau,
+            keep_ratio=self.keep_ratio, drop_uniform=base.drop_uniform,
+            slab_tokens=slab_tokens, status=status, dhidden_dtype=dhidden_dtype)
+
+
+def onehot_parts(H, W, y, g):
+    """The sparse parts of the LM-head gradient: g_t W[y_t] (dH) and the scatter of
+    g_t H_t onto row y_t (dW)."""
+    dH1 = g[:, None] * W[y]
+    dW1 = np.zeros_like(W)
+    np.add.at(dW1, y, g[:, None] * H)
+    return dH1, dW1
+
+
+def check_grads(H, W, y, g_ref, dH_gpu, dW_gpu, dH_ref, dW_ref, rel=REL):
+    """Whole-gradient relative Frobenius error, and the same for the softmax part alone
+    (the dense GEMM part; the one-hot part dominates the norm)."""
+    out = {}
+    if dH_gpu is not None:
+        out["dH"] = rel_fro(dH_gpu, dH_ref)
+        dH1, _ = onehot_parts(H, W, y, g_ref)
+        out["dH_soft"] = rel_fro(dH_gpu - dH1, dH_ref - dH1)
+    if dW_gpu is not None:
+        out["dW"] = rel_fro(dW_gpu, dW_ref)
+        _, dW1 = onehot_parts(H, W, y, g_ref)
+        out["dW_soft"] = rel_fro(dW_gpu - dW1, dW_ref - dW1)
+    for k, v in out.items():
+        assert v <= rel, (k, v, out)
+    return out

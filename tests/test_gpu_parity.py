@@ -1,0 +1,249 @@
+"""GPU parity of the HIP path (called through the C ABI) against the fp64 oracle on the
+same seeded inputs, at sizes the oracle finishes in seconds that still span several
+256-wide tiles with ragged tails.  Bars: masks / indices / offsets bit-exact; log-probs
+2e-3 absolute; loss and gradients 1e-2 relative (also for the softmax part of the
+gradients alone)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import CONFIGS, make_rollouts
+from tests._parity import (Problem, to_dev, rel_fro, check_grads, LOGP_ATOL, REL)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fr():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_36932_amd as m
+    return m
+
+
+DEV = "cuda:0"
+
+
+def _status():
+    return torch.zeros(1, dtype=torch.int32, device=DEV)
+
+
+@pytest.mark.parametrize("c", [1, 2, 3, 4, 5])
+def test_advantage(fr, c):
+    ro = make_rollouts(CONFIGS[c])
+    cfg = CONFIGS[c]
+    adv, cls, valid = oracle.group_advantage(ro.rewards, ro.group_off,
+                                             drop_uniform=cfg.drop_uniform)
+    st = _status()
+    a, k, v = fr.advantage(to_dev(ro.rewards, DEV), to_dev(ro.group_off, DEV),
+                           drop_uniform=cfg.drop_uniform, status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0
+    np.testing.assert_allclose(a.cpu().numpy(), adv, rtol=1e-6, atol=1e-6)
+    assert np.array_equal(k.cpu().numpy(), cls)
+    assert np.array_equal(v.cpu().numpy(), valid)
+
+
+def _prune_gpu(fr, ro, cls, valid, V, n, tau, keep):
+    st = _status()
+    out = fr.prune(to_dev(ro.token_ids, DEV), to_dev(ro.traj_tok_off, DEV),
+                   to_dev(ro.rewards, DEV), to_dev(ro.group_off, DEV), to_dev(cls, DEV),
+                   to_dev(valid, DEV), V=V, max_group=int(np.diff(ro.group_off).max()),
+                   max_len=int(ro.lengths.max()), ngram_n=n, tau=tau, keep_ratio=keep,
+                   status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0, fr.status_names(st.item())
+    return out
+
+
+def _check_prune(out, ref, N):
+    assert np.array_equal(out["keep_mask"].cpu().numpy(), ref["keep_mask"])
+    assert np.array_equal(out["mdap_count"].cpu().numpy(), ref["mdap_count"])
+    nk, tk = out["counts"].cpu().tolist()
+    assert nk == len(ref["kept_traj"]) and tk == len(ref["tok_src"])
+    assert np.array_equal(out["kept_traj"][:nk].cpu().numpy(), ref["kept_traj"])
+    assert np.array_equal(out["kept_tok_off"][:nk + 1].cpu().numpy(), ref["kept_tok_off"])
+    assert np.array_equal(out["tok_src"][:tk].cpu().numpy(), ref["tok_src"])
+
+
+@pytest.mark.parametrize("c", [1, 2, 3, 4, 5])
+def test_prune_full_config(fr, c):
+    """Pruning, budget and compaction at each workload's full size: bit-exact."""
+    cfg = CONFIGS[c]
+    ro = make_rollouts(cfg)
+    ref = oracle.hot_path_step(ro.rewards, ro.group_off, ro.token_ids, ro.traj_tok_off,
+                               lmhead=False, keep_ratio=cfg.keep_ratio,
+                               drop_uniform=cfg.drop_uniform)
+    out = _prune_gpu(fr, ro, ref["class_id"], ref["group_valid"], cfg.V, 1, (4, 5),
+                     cfg.keep_ratio)
+    _check_prune(out, ref, ro.N)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3])
+@pytest.mark.parametrize("tau", [(4, 5), (0, 1), (2, 1), (1, 1), (1, 2)])
+@pytest.mark.parametrize("keep", [0.0, 0.5])
+def test_prune_planted_duplicates(fr, n, tau, keep):
+    """Near-duplicate rollouts inside each question so the Jaccard test actually prunes."""
+    from synth import plant_duplicates
+    cfg = CONFIGS[5]
+    ro = make_rollouts(cfg, Q=24, len_range=(1, 40), V=40, seed=123 + n)
+    plant_duplicates(ro, p_copy=0.7, p_mutate=0.2, seed=n)
+    ref = oracle.hot_path_step(ro.rewards, ro.group_off, ro.token_ids, ro.traj_tok_off,
+                               lmhead=False, ngram_n=n, tau_num=tau[0], tau_den=tau[1],
+                               keep_ratio=keep)
+    out = _prune_gpu(fr, ro, ref["class_id"], ref["group_valid"], 40, n, tau, keep)
+    _check_prune(out, ref, ro.N)
+    if tau == (4, 5) and keep == 0.0:
+        assert ref["keep_mask"].sum() < ro.N  # the planted duplicates were pruned
+
+
+def test_prune_bad_token_flags_status(fr):
+    cfg = CONFIGS[1]
+    ro = make_rollouts(cfg)
+    ro.token_ids[5] = cfg.V + 3
+    ref = oracle.group_advantage(ro.rewards, ro.group_off)
+    st = _status()
+    fr.prune(to_dev(ro.token_ids, DEV), to_dev(ro.traj_tok_off, DEV), to_dev(ro.rewards, DEV),
+             to_dev(ro.group_off, DEV), to_dev(ref[1], DEV), to_dev(ref[2], DEV), V=cfg.V,
+             max_group=8, max_len=64, keep_ratio=0.5, status=st)
+    torch.cuda.synchronize()
+    assert st.item() & 0x2
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("V,d", [(1000, 64), (4096, 256), (777, 136)])
+def test_token_logprob(fr, dtype, V, d):
+    rng = np.random.default_rng(V + d)
+    T = 613
+    H = rng.normal(size=(T, d)).astype(np.float32)
+    W = (0.05 * rng.normal(size=(V, d))).astype(np.float32)
+    if dtype == "bf16":
+        Ht, Wt = torch.from_numpy(H).bfloat16(), torch.from_numpy(W).bfloat16()
+    else:
+        Ht, Wt = torch.from_numpy(H), torch.from_numpy(W)
+    y = rng.integers(0, V, size=T).astype(np.int32)
+    # a gather through row_index (every other row, reversed)
+    rows = np.arange(T)[::-2].astype(np.int32).copy()
+    lp_ref, lse_ref = oracle.token_logprob(Ht.double().numpy()[rows], Wt.double().numpy(),
+                                           y[rows])
+    st = _status()
+    lp, lse = fr.token_logprob(Ht.to(DEV), Wt.to(DEV), to_dev(y, DEV), row_index=to_dev(rows, DEV),
+                               status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0
+    assert np.abs(lp.cpu().numpy() - lp_ref).max() < LOGP_ATOL
+    assert np.abs(lse.cpu().numpy() - lse_ref).max() < LOGP_ATOL
+
+
+CASES = {
+    # cfg id, overrides
+    "grpo_kl_bf16": (3, dict(Q=6, len_range=(20, 90), V=1000, d=136)),
+    "dapo_bf16": (4, dict(Q=5, len_range=(10, 120), V=1291, d=64)),
+    "gspo_bf16": (5, dict(Q=6, len_range=(30, 100), V=900, d=96)),
+    "grpo_tokmean_bf16": (2, dict(Q=6, len_range=(5, 70), V=600, d=128)),
+    "grpo_f32": (1, dict(Q=4, len_range=(16, 64), V=1500, d=72)),
+    "gspo_f32": (5, dict(Q=4, len_range=(8, 60), V=700, d=64, dtype="f32")),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+@pytest.mark.parametrize("slab", [0, 150])
+def test_hot_path_small(fr, case, slab):
+    c, kw = CASES[case]
+    pb = Problem(c, DEV, **kw)
+    ref = pb.oracle_loss()
+    st = _status()
+    out = pb.run_gpu(fr, slab_tokens=slab, status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0, fr.status_names(st.item())
+    assert np.array_equal(out["prune"]["keep_mask"].cpu().numpy(), pb.pr["keep_mask"])
+    call = out["call"]
+    T = out["t_kept"]
+    assert T == len(pb.src)
+    lp = call.logp[:T].double().cpu().numpy()
+    assert np.abs(lp - pb.logp_exact).max() < LOGP_ATOL
+    assert np.abs(call.lse[:T].double().cpu().numpy() - pb.lse_exact).max() < LOGP_ATOL
+    loss = float(call.loss.item())
+    scale = max(abs(ref["loss"]), 1e-3 * np.abs(ref["g"]).sum() / max(T, 1))
+    assert abs(loss - ref["loss"]) <= REL * max(abs(ref["loss"]), 1e-12), (loss, ref["loss"])
+    assert int(call.stats[0].item()) == ref["clipped"]
+    Hk = pb.H64[pb.src]
+    errs = check_grads(Hk, pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
+                       call.dW.double().cpu().numpy(), ref["dH"], ref["dW"])
+    print(case, slab, errs)
+
+
+def test_cfg1_full(fr):
+    """The tiny fp32 workload end to end at its full size."""
+    pb = Problem(1, DEV)
+    ref = pb.oracle_loss()
+    st = _status()
+    out = pb.run_gpu(fr, status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0
+    call = out["call"]
+    T = out["t_kept"]
+    assert np.abs(call.logp[:T].double().cpu().numpy() - pb.logp_exact).max() < 1e-4
+    assert abs(call.loss.item() - ref["loss"]) <= 1e-4 * abs(ref["loss"])
+    check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
+                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"], rel=1e-4)
+
+
+def test_large_logits_take_the_shifted_path(fr):
+    """Logits far outside exp's float range: rows are re-evaluated with a per-row shift and
+    the results still match."""
+    pb = Problem(3, DEV, Q=3, len_range=(20, 60), V=700, d=64, h_std=40.0, w_std=0.2)
+    ref = pb.oracle_loss()
+    st = _status()
+    out = pb.run_gpu(fr, status=st)
+    torch.cuda.synchronize()
+    call = out["call"]
+    T = out["t_kept"]
+    assert call.stats[1].item() > 0  # some rows needed the shift
+    assert np.abs(call.logp[:T].double().cpu().numpy() - pb.logp_exact).max() < LOGP_ATOL * 50
+    check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
+                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"])
+
+
+def test_deterministic(fr):
+    pb = Problem(5, DEV, Q=4, len_range=(30, 80), V=800, d=64)
+    a = pb.run_gpu(fr)
+    b = pb.run_gpu(fr)
+    torch.cuda.synchronize()
+    nk, tk = a["n_kept"], a["t_kept"]
+    assert (nk, tk) == (b["n_kept"], b["t_kept"])
+    valid = {"keep_mask": None, "kept_traj": nk, "kept_tok_off": nk + 1, "tok_src": tk}
+    for k, n in valid.items():  # entries past the counts are undefined by contract
+        assert torch.equal(a["prune"][k][:n], b["prune"][k][:n])
+    assert torch.equal(a["call"].loss, b["call"].loss)
+    assert torch.equal(a["call"].dW, b["call"].dW)
+    assert torch.equal(a["call"].dhidden, b["call"].dhidden)
+
+
+def test_empty_and_single_token(fr):
+    # no kept sequence at all: loss 0, dW zero
+    d, V = 64, 300
+    H = torch.randn(4, d).bfloat16().to(DEV)
+    W = (0.02 * torch.randn(V, d)).bfloat16().to(DEV)
+    z = torch.zeros(1, dtype=torch.int64)
+    call = fr.policy_loss_fwd_bwd(H, W, torch.zeros(4, dtype=torch.int32, device=DEV),
+                                  torch.zeros(4, device=DEV), z.to(DEV), z,
+                                  torch.zeros(1, device=DEV), need_dhidden=True)
+    torch.cuda.synchronize()
+    assert call.loss.item() == 0.0 and torch.count_nonzero(call.dW).item() == 0
+    # one sequence of one token against the oracle
+    y = np.asarray([7], dtype=np.int32)
+    Hn = H[:1].double().cpu().numpy()
+    Wn = W.double().cpu().numpy()
+    lp, lse = oracle.token_logprob(Hn, Wn, y)
+    old = (lp - 0.1).astype(np.float32)
+    off = np.asarray([0, 1], dtype=np.int64)
+    loss, g, _ = oracle.policy_loss(lp, old.astype(np.float64), None, off, [0.7])
+    dH, dW = oracle.lmhead_backward(Hn, Wn, y, lse, g)
+    call = fr.policy_loss_fwd_bwd(H[:1].contiguous(), W, to_dev(y, DEV), to_dev(old, DEV),
+                                  to_dev(off, DEV), torch.from_numpy(off),
+                                  torch.tensor([0.7], device=DEV))
+    torch.cuda.synchronize()
+    assert abs(call.loss.item() - loss) < 1e-2 * abs(loss)
+    assert rel_fro(call.dW.double().cpu().numpy(), dW) < REL
+    assert rel_fro(call.dhidden[:1].double().cpu().numpy(), dH) < REL

@@ -1,0 +1,148 @@
+"""Host-side checks of libfastrl that need no GPU: the library loads, exports every
+function include/fastrl.h declares, rejects bad arguments before enqueuing anything,
+and its host-only ARS controller agrees with the oracle's."""
+import ctypes
+import json
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fastrl.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fastrl_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def fr():
+    import paper_2609_36932_amd as m
+    return m
+
+
+def test_exports_every_declared_symbol(fr):
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(fr._lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", fr.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    exported = set(re.findall(r"\bT (fastrl_\w+)", out))
+    assert set(names) <= exported, set(names) - exported
+
+
+def test_struct_layout(fr):
+    assert fr._lib.fastrl_loss_args_size() == ctypes.sizeof(fr.LossArgs)
+    assert fr._lib.fastrl_version() >= 10000
+
+
+def test_host_validation_errors(fr):
+    L = fr._lib
+    assert L.fastrl_advantage(None, None, -1, 0, 1, 1e-6, 0, None, None, None, None, None) == -2
+    assert L.fastrl_advantage(None, None, 1, 1, 2, 1e-6, 0, None, None, None, None, None) == -3
+    assert L.fastrl_advantage(None, None, 1, 1, 1, 1e-6, 0, None, None, None, None, None) == -1
+    assert b"group_off" in L.fastrl_last_error()
+    # empty question set: a no-op that succeeds without touching the device
+    assert L.fastrl_advantage(None, None, 0, 0, 1, 1e-6, 0, None, None, None, None, None) == 0
+    args = [None, None, 10, None, None, None, None, 2, 16, 8, 64, 1000, 1, 4, 5, 0.5,
+            None, None, None, None, None, None, None, None, 0, None]
+    a = list(args); a[12] = 4                     # ngram_n
+    assert L.fastrl_prune(*a) == -3
+    a = list(args); a[11] = 1 << 21               # V
+    assert L.fastrl_prune(*a) == -3
+    a = list(args); a[14] = 0                     # tau_den
+    assert L.fastrl_prune(*a) == -3
+    a = list(args); a[9] = 300                    # max_group
+    assert L.fastrl_prune(*a) == -2
+    a = list(args); a[15] = 1.5                   # keep_ratio
+    assert L.fastrl_prune(*a) == -3
+    assert L.fastrl_prune(*args) == -1            # NULL arrays
+    # dtype / shape checks of the LM-head entry points
+    assert L.fastrl_token_logprob(None, None, None, 7, 1, 16, 10, None, None, None, None,
+                                  None, 0, None) == -4
+    assert L.fastrl_token_logprob(None, None, None, 1, 1, 12, 10, None, None, None, None,
+                                  None, 0, None) == -2
+    a = fr.LossArgs()
+    a.dtype, a.d, a.V, a.S, a.T = 1, 64, 100, 0, 0
+    assert L.fastrl_policy_loss_fwd_bwd(ctypes.byref(a), None) == -1   # seq_off NULL
+    a.algo = 9
+    assert L.fastrl_policy_loss_fwd_bwd(ctypes.byref(a), None) == -3
+    a.algo, a.dtype = 0, 3
+    assert L.fastrl_policy_loss_fwd_bwd(ctypes.byref(a), None) == -4
+
+
+def test_workspace_queries(fr):
+    L = fr._lib
+    assert L.fastrl_prune_workspace_size(4, 32, 1000, 8, 1) >= 1000 * 8
+    assert L.fastrl_token_logprob_workspace_size(1000, 256, 4096, 0) > 0
+    off = np.asarray([0, 100, 250], dtype=np.int64)
+    a = fr.LossArgs()
+    a.dtype, a.d, a.V, a.S, a.T = 1, 3584, 152064, 2, 250
+    a.seq_off = ctypes.c_void_p(1)
+    a.seq_off_host = ctypes.c_void_p(off.ctypes.data)
+    a.loss = a.hidden = a.W = a.token_ids = a.old_logp = a.adv = ctypes.c_void_p(256)
+    a.dhidden = a.dW = ctypes.c_void_p(256)
+    a.dhidden_dtype = 0
+    n = L.fastrl_policy_loss_workspace_size(ctypes.byref(a))
+    Vp = 152064
+    # two [slab, V] bf16 buffers for a 256-token slab, plus the transposed W
+    assert n >= 2 * 256 * Vp * 2 + 3584 * Vp * 2
+
+
+def test_ars_matches_oracle(fr, golden_dir):
+    from oracle import ARSController
+    d = json.load(open(os.path.join(golden_dir, "ars_sequence.json")))
+    for run in d["runs"]:
+        c = fr.ARS(run["G"], run["M"], run["E"])
+        ns = []
+        for counts in run["steps"]:
+            ns.append(c.next_n())
+            c.observe(counts)
+        assert ns == run["n_before_step"] and c.next_n() == run["n_after"]
+    rng = np.random.default_rng(0)
+    for _ in range(50):
+        G = int(rng.choice([4, 8, 16]))
+        E = int(rng.integers(1, 4))
+        M = E * int(rng.integers(1, 6))
+        a, b = ARSController(G, M, E), fr.ARS(G, M, E)
+        for step in range(M + 2):
+            assert a.next_n() == b.next_n()
+            counts = list(rng.integers(1, G + 1, size=int(rng.integers(1, 9))))
+            valid = list(rng.integers(0, 2, size=len(counts)))
+            a.observe([c for c, v in zip(counts, valid) if v])
+            b.observe(counts, valid)
+            if a.G_t is not None:
+                assert a.G_t == b.state.G_t and a.G_ref == b.state.G_ref
+
+
+def test_ars_checkpoint_roundtrip(fr):
+    rng = np.random.default_rng(5)
+    steps = [list(rng.integers(1, 9, size=6)) for _ in range(12)]
+    full = fr.ARS(8, 12, 3)
+    ns_full = []
+    for c in steps:
+        ns_full.append(full.next_n())
+        full.observe(c)
+    part = fr.ARS(8, 12, 3)
+    ns = []
+    for c in steps[:5]:
+        ns.append(part.next_n())
+        part.observe(c)
+    blob = part.to_bytes()
+    resumed = fr.ARS.from_bytes(blob)
+    for c in steps[5:]:
+        ns.append(resumed.next_n())
+        resumed.observe(c)
+    assert ns == ns_full and resumed.to_bytes() == full.to_bytes()
+
+
+def test_ars_bad_args(fr):
+    st = fr.ARSState()
+    assert fr._lib.fastrl_ars_init(ctypes.byref(st), 1, 10, 2) == -3
+    assert fr._lib.fastrl_ars_init(None, 8, 10, 2) == -1
