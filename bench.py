@@ -1,0 +1,207 @@
+"""Benchmark of one FastRL GRPO hot-path step on one MI355X.
+
+A step is the whole hot path over one batch of seeded synthetic rollouts shaped like
+the Qwen2.5-VL-7B GRPO setting (64 prompts x G=8 rollouts, response lengths
+U[128, 1024], d = 3584, V = 152064, bf16 hidden/W, KL to a reference at beta = 0.04,
+clip 0.2, keep ratio 0.5):
+
+  fastrl_advantage -> fastrl_prune (MDAP + budget + compaction) -> read the kept counts
+  -> fastrl_policy_loss_fwd_bwd on the kept tokens (logits GEMM with online log-sum-exp,
+  loss, dhidden and dW GEMMs).
+
+Inputs are resident in HBM before timing.  The reported value is kept tokens per second
+of the whole step.  ``roofline`` describes the dominant kernel, timed with HIP events on
+its launch stream during the timed steps; ``cpu_baseline`` times the fp64 oracle on a
+bounded sample of the same workload.
+
+usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 3] [--no-cpu]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 MFMA
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--slab", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=768)
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def make_inputs(cfg, dev, fr):
+    import torch
+    from synth import make_rollouts, make_dense
+    ro = make_rollouts(cfg)
+    H, W = make_dense(cfg, ro.T_total, device=dev)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+    inp = dict(rewards=t(ro.rewards), group_off=t(ro.group_off), token_ids=t(ro.token_ids),
+               traj_tok_off=t(ro.traj_tok_off), H=H, W=W)
+    # old / ref log-probs = current log-probs + N(0, 0.05): evaluate the current policy's
+    # log-probs of the kept tokens once, untimed, with the library itself
+    adv, cls, valid = fr.advantage(inp["rewards"], inp["group_off"],
+                                   drop_uniform=cfg.drop_uniform)
+    pr = fr.prune(inp["token_ids"], inp["traj_tok_off"], inp["rewards"], inp["group_off"],
+                  cls, valid, V=cfg.V, max_group=int(np.diff(ro.group_off).max()),
+                  max_len=int(ro.lengths.max()), keep_ratio=cfg.keep_ratio)
+    tk = int(pr["counts"][1].item())
+    src = pr["tok_src"][:tk]
+    lp, _ = fr.token_logprob(H, W, inp["token_ids"], row_index=src)
+    old = torch.full((ro.T_total,), float("nan"), device=dev)
+    ref = torch.full((ro.T_total,), float("nan"), device=dev)
+    srcl = src.long()
+    old[srcl] = lp + t(ro.old_noise)[srcl].float()
+    ref[srcl] = lp + t(ro.ref_noise)[srcl].float()
+    inp.update(old=old, ref=ref if cfg.beta else None)
+    torch.cuda.synchronize()
+    return ro, inp
+
+
+def cpu_baseline(cfg, ro, inp, n_tokens):
+    """The oracle, as it stands, on a bounded sample: advantage + pruning + compaction of
+    the whole batch, then the LM-head forward, loss and full backward (dH and dW at full
+    V x d) for the first kept sequences holding >= n_tokens tokens."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    H = inp["H"]
+    Wd = inp["W"].float().cpu().numpy().astype(np.float64)
+    old = inp["old"].cpu().numpy()
+    ref = inp["ref"].cpu().numpy() if inp["ref"] is not None else None
+    t0 = time.perf_counter()
+    pr = oracle.hot_path_step(ro.rewards, ro.group_off, ro.token_ids, ro.traj_tok_off,
+                              lmhead=False, keep_ratio=cfg.keep_ratio,
+                              drop_uniform=cfg.drop_uniform)
+    koff = pr["kept_tok_off"]
+    S = int(np.searchsorted(koff, n_tokens)) if koff[-1] >= n_tokens else len(koff) - 1
+    S = max(1, min(S, len(koff) - 1))
+    src = pr["tok_src"][:koff[S]]
+    Hk = H[torch_index(src, H.device)].float().cpu().numpy().astype(np.float64)
+    y = ro.token_ids[src].astype(np.int64)
+    logp, lse = oracle.token_logprob(Hk, Wd, y)
+    loss, g, _ = oracle.policy_loss(logp, old[src].astype(np.float64),
+                                    None if ref is None else ref[src].astype(np.float64),
+                                    koff[:S + 1], pr["adv"][pr["kept_traj"][:S]],
+                                    algo=cfg.algo, norm=cfg.norm, eps_low=cfg.eps_low,
+                                    eps_high=cfg.eps_high, beta=cfg.beta)
+    dH, dW = oracle.lmhead_backward(Hk, Wd, y, lse, g)
+    dt = time.perf_counter() - t0
+    return dict(value=len(src) / dt, unit="kept tokens/s", cores=int(cores), kind="oracle",
+                sample=f"whole batch advantage+MDAP+compaction, then LM-head fwd + loss + "
+                       f"full bwd (dH, dW at V={cfg.V}, d={cfg.d}) in fp64 for the first "
+                       f"{S} kept sequences ({len(src)} tokens); {dt:.1f} s")
+
+
+def torch_index(src, dev):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(src)).long().to(dev)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path is "
+              "built for one MI355X and multi-GPU sharding is a design note, not a run.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_36932_amd as fr
+    from synth import CONFIGS
+    cfg = CONFIGS[args.workload]
+    dev = torch.device("cuda:0")
+    log(f"[bench] workload {cfg.name}: generating inputs")
+    ro, inp = make_inputs(cfg, dev, fr)
+    max_group = int(np.diff(ro.group_off).max())
+    max_len = int(ro.lengths.max())
+
+    def step():
+        return fr.hot_path_step(
+            inp["rewards"], inp["group_off"], inp["token_ids"], inp["traj_tok_off"],
+            inp["H"], inp["W"], inp["old"], inp["ref"], V=cfg.V, max_group=max_group,
+            max_len=max_len, algo=cfg.algo, norm=cfg.norm, eps_low=cfg.eps_low,
+            eps_high=cfg.eps_high, beta=cfg.beta, ngram_n=cfg.ngram_n,
+            tau=(cfg.tau_num, cfg.tau_den), keep_ratio=cfg.keep_ratio,
+            drop_uniform=cfg.drop_uniform, slab_tokens=args.slab)
+
+    for i in range(args.warmup):
+        out = step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    fr.profile_reset()
+    fr.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    kept = 0
+    for i in range(args.steps):
+        out = step()
+        kept += out["t_kept"]
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    fr.profile_enable(False)
+    log(f"[bench] {args.steps} timed steps in {elapsed:.3f} s")
+    kinds = {fr.K_LOGITS_FWD: "logits_fwd", fr.K_DHIDDEN: "dhidden", fr.K_DW: "dW"}
+    per = {}
+    for k, name in kinds.items():
+        ms, n, fl = fr.profile_read(k)
+        if n:
+            per[name] = dict(ms_total=ms, launches=n, tflops=fl / (ms * 1e-3) / 1e12,
+                             avg_ms=ms / n, flops_per_launch=fl / n)
+    dom = max(per, key=lambda k: per[k]["ms_total"])
+    peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
+    ach = per[dom]["tflops"]
+    t_kept = out["t_kept"]
+    gemm_ms = sum(v["ms_total"] for v in per.values()) / args.steps
+    useful = 6.0 * cfg.V * cfg.d * t_kept / (elapsed / args.steps) / 1e12
+    res = {
+        "metric": "kept tokens/s for log-prob+loss fwd/bwd at 7B LM-head shape; % bf16 MFMA peak",
+        "value": kept / elapsed,
+        "unit": "kept tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded rollouts; random-init bf16 hidden states and LM-head weights)",
+        "config": {"workload": f"{cfg.name}: {cfg.Q} prompts x G={cfg.G[0]}, lengths "
+                               f"U[{cfg.len_lo},{cfg.len_hi}], d={cfg.d}, V={cfg.V}, "
+                               f"keep ratio {cfg.keep_ratio}, beta {cfg.beta}",
+                   "kept_tokens_per_step": t_kept, "kept_sequences": out["n_kept"],
+                   "total_tokens": ro.T_total, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": ach, "peak": peak,
+                     "unit": "TFLOP/s", "frac": ach / peak, "traffic": None},
+        "useful_frac_of_step": useful / peak,
+        "kernels": per,
+        "gemm_ms_per_step": gemm_ms,
+    }
+    if not args.no_cpu:
+        log("[bench] timing the oracle on a CPU sample")
+        res["cpu_baseline"] = cpu_baseline(cfg, ro, inp, args.cpu_tokens)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -19,7 +19,8 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libfastrl.so")
+# FASTRL_LIB selects another build of the same library (e.g. a debug build)
+LIB_PATH = os.environ.get("FASTRL_LIB", os.path.join(_HERE, "libfastrl.so"))
 
 F32, BF16 = 0, 1
 GRPO, DAPO, GSPO = 0, 1, 2

@@ -144,29 +144,159 @@ __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
   return wn * 128 + ni * 32 + (lane & 31);
 }
 
-template <typename T, int MODE>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void lm_gemm_kernel(const GemmParams p) {
-  using E = Eng<T>;
-  constexpr int BK = E::BK, LD = E::LD, VEC = E::VEC;
-  constexpr int VPR = BK / VEC;                       // vectors per tile row
-  constexpr int LOADS = kBM * VPR / kThreads;         // vectors per thread per operand
-  __shared__ __attribute__((aligned(16))) T smem[2 * 2 * kBM * LD];
-  T* As = smem;
-  T* Bs = smem + 2 * kBM * LD;
+typedef __attribute__((address_space(3))) void lds_void_t;
 
-  int mb, nb;
-  tile_coords(mb, nb, p.nmb, p.nnb);
-  if (MODE == MODE_FWD && p.store_e == 2 && p.redo_blk[nb] == 0) return;
-  const int m0 = mb * kBM, n0 = nb * kBN;
+// bf16 main loop.  LDS holds two stages of a 256 x 64 A tile and a 256 x 64 B tile
+// (32 KB each), written by direct global->LDS loads (global_load_lds_dwordx4): one load
+// instruction moves 8 rows x 128 B, lane l writing the 16-byte slot l of that 1 KB.  Row r
+// keeps its k-chunk c (8 bf16) in slot c ^ ((r >> 1) & 7): the LDS serves a 16-byte-per-lane
+// read 16 lanes (256 B, 64 banks) at a time, and rows r..r+15 of a fragment then land on 16
+// distinct 16-byte bank groups (two rows share each 256 B line, parity picks the half).
+// Tile kt+2 is fetched while tile kt is multiplied; fragments of k-step kk+1 are read while
+// the MFMAs of k-step kk run.
+template <int MODE>
+__device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n0,
+                                              f32x16_t (&acc)[4][4], uint16_t* smem) {
+  constexpr int BK = 64;
+  constexpr int TILE = kBM * BK;  // elements per operand per stage
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const uint16_t* Ag = static_cast<const uint16_t*>(p.A);
+  const uint16_t* Bg = static_cast<const uint16_t*>(p.B);
+  const int lrow = lane >> 3;
+  // global k-chunk this lane moves into its slot; rows r0 + lrow with r0 = 8 (8 wave + j),
+  // so ((r >> 1) & 7) = 4 (j & 1) + (lrow >> 1)
+  const int gch[2] = {(lane & 7) ^ (lrow >> 1), (lane & 7) ^ (4 | (lrow >> 1))};
+  int64_t arow[8], brow[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int r = wave * 64 + j * 8 + lrow;
+    const int ra = min(m0 + r, p.M - 1);   // rows past the edge load a valid row; their
+    arow[j] = int64_t(ra) * p.lda;         // results are never stored
+    const int rb = min(n0 + r, p.N - 1);
+    int64_t br = rb;
+    if (MODE == MODE_FWD) {
+      br += p.b_row_base;
+      if (p.b_rows) br = p.b_rows[br];
+    }
+    brow[j] = br * p.ldb;
+  }
+  const int K = p.K;
+  const int nk = (K + BK - 1) / BK;
+  const bool ktail = (K % BK) != 0;
+  auto issue = [&](int kt, int stage) {
+    // clamp the chunk so a partial last tile never reads past the end of a row
+    const int kc0 = min(kt * BK + gch[0] * 8, K - 8);
+    const int kc1 = min(kt * BK + gch[1] * 8, K - 8);
+    uint16_t* sa = smem + stage * 2 * TILE + wave * 64 * BK;
+    uint16_t* sb = sa + TILE;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int kc = (j & 1) ? kc1 : kc0;
+      __builtin_amdgcn_global_load_lds(Ag + arow[j] + kc, (lds_void_t*)(sa + j * 8 * BK), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(Bg + brow[j] + kc, (lds_void_t*)(sb + j * 8 * BK), 16, 0, 0);
+    }
+  };
+  auto zero_tail = [&](int kt, int stage) {  // this lane's slots past K in tile kt
+    uint16_t* sa = smem + stage * 2 * TILE + wave * 64 * BK + lane * 8;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (kt * BK + gch[j & 1] * 8 >= K) {
+        *reinterpret_cast<u32x4_t*>(sa + j * 8 * BK) = u32x4_t{0u, 0u, 0u, 0u};
+        *reinterpret_cast<u32x4_t*>(sa + TILE + j * 8 * BK) = u32x4_t{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+  const int sw = (lane >> 1) & 7;  // ((row >> 1) & 7) of the fragment rows this lane reads
+  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[4]) {
+    const uint16_t* as = smem + stage * 2 * TILE;
+    const uint16_t* bs = as + TILE;
+    const int slot = ((kk * 2 + (lane >> 5)) ^ sw) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 32 + (lane & 31)) * BK + slot);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 128 + j * 32 + (lane & 31)) * BK + slot);
+  };
+  auto mma = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
+
+  bf16x8_t fa0[4], fb0[4], fa1[4], fb1[4];
+  // pin the order inside a k-step: the 16 MFMAs of this step with the 8 fragment reads of
+  // the next step spread among them (at most 8 LDS reads in flight, so the wait before the
+  // next step's MFMAs is exact, and the last read still has 8 MFMAs to land)
+#define FR_STEP_ORDER()                                  \
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);     \
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);     \
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);     \
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);     \
+  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);     \
+  __builtin_amdgcn_sched_barrier(0)
+  issue(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (nk == 1 && ktail) zero_tail(0, 0);
+  __syncthreads();
+  frags(0, 0, fa0, fb0);
+  if (nk > 1) issue(1, 1);
+  int kt = 0;
+  for (; kt + 1 < nk; ++kt) {
+    const int cur = kt & 1;
+    frags(cur, 1, fa1, fb1);
+    mma(fa0, fb0);
+    FR_STEP_ORDER();
+    frags(cur, 2, fa0, fb0);
+    mma(fa1, fb1);
+    FR_STEP_ORDER();
+    frags(cur, 3, fa1, fb1);
+    mma(fa0, fb0);
+    FR_STEP_ORDER();
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tile kt+1 is in LDS
+    if (kt + 2 == nk && ktail) zero_tail(kt + 1, cur ^ 1);
+    __syncthreads();                                   // and nobody reads tile kt any more
+    if (kt + 2 < nk) issue(kt + 2, cur);
+    frags(cur ^ 1, 0, fa0, fb0);
+    mma(fa1, fb1);
+    FR_STEP_ORDER();
+  }
+  {  // last tile
+    const int cur = kt & 1;
+    frags(cur, 1, fa1, fb1);
+    mma(fa0, fb0);
+    FR_STEP_ORDER();
+    frags(cur, 2, fa0, fb0);
+    mma(fa1, fb1);
+    FR_STEP_ORDER();
+    frags(cur, 3, fa1, fb1);
+    mma(fa0, fb0);
+    FR_STEP_ORDER();
+    mma(fa1, fb1);
+  }
+#undef FR_STEP_ORDER
+}
+
+// float32 main loop (small problems): register-staged loads into padded LDS rows
+template <int MODE>
+__device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0,
+                                             f32x16_t (&acc)[4][4], float* smem) {
+  using E = Eng<float>;
+  constexpr int BK = E::BK, LD = E::LD, VEC = E::VEC;
+  constexpr int VPR = BK / VEC;
+  constexpr int LOADS = kBM * VPR / kThreads;
+  float* As = smem;
+  float* Bs = smem + 2 * kBM * LD;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-
-  const T* Ag = static_cast<const T*>(p.A);
-  const T* Bg = static_cast<const T*>(p.B);
-  // per-thread global source rows (fixed for the whole K loop)
-  const T* arow[LOADS];
-  const T* brow[LOADS];
+  const float* Ag = static_cast<const float*>(p.A);
+  const float* Bg = static_cast<const float*>(p.B);
+  const float* arow[LOADS];
+  const float* brow[LOADS];
   bool aok[LOADS], bok[LOADS];
   int kofs[LOADS], srow[LOADS];
 #pragma unroll
@@ -187,13 +317,6 @@ void lm_gemm_kernel(const GemmParams p) {
     }
     brow[j] = Bg + br * p.ldb;
   }
-
-  f32x16_t acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
-
   u32x4_t ra[LOADS], rb[LOADS];
   const int nk = (p.K + BK - 1) / BK;
   auto gload = [&](int kt) {
@@ -201,8 +324,8 @@ void lm_gemm_kernel(const GemmParams p) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       const int k = k0 + kofs[j];
-      load_vec<T>(arow[j] + k, aok[j] && k < p.K, ra[j]);
-      load_vec<T>(brow[j] + k, bok[j] && k < p.K, rb[j]);
+      load_vec<float>(arow[j] + k, aok[j] && k < p.K, ra[j]);
+      load_vec<float>(brow[j] + k, bok[j] && k < p.K, rb[j]);
     }
   };
   auto sstore = [&](int buf) {
@@ -212,52 +335,58 @@ void lm_gemm_kernel(const GemmParams p) {
       *reinterpret_cast<u32x4_t*>(Bs + (buf * kBM + srow[j]) * LD + kofs[j]) = rb[j];
     }
   };
-
   gload(0);
   sstore(0);
   for (int kt = 0; kt < nk; ++kt) {
     __syncthreads();
     const int buf = kt & 1;
     if (kt + 1 < nk) gload(kt + 1);
-    const T* as = As + buf * kBM * LD;
-    const T* bs = Bs + buf * kBM * LD;
-    if constexpr (sizeof(T) == 2) {
+    const float* as = As + buf * kBM * LD;
+    const float* bs = Bs + buf * kBM * LD;
 #pragma unroll
-      for (int kk = 0; kk < BK; kk += 16) {
-        bf16x8_t af[4], bf[4];
-        const int kq = kk + (lane >> 5) * 8;
+    for (int kk = 0; kk < BK; kk += 2) {
+      float af[4], bf[4];
+      const int kq = kk + (lane >> 5);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          af[i] = *reinterpret_cast<const bf16x8_t*>(
-              as + (wm * 128 + i * 32 + (lane & 31)) * LD + kq);
+      for (int i = 0; i < 4; ++i) af[i] = as[(wm * 128 + i * 32 + (lane & 31)) * LD + kq];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bf[j] = bs[(wn * 128 + j * 32 + (lane & 31)) * LD + kq];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          bf[j] = *reinterpret_cast<const bf16x8_t*>(
-              bs + (wn * 128 + j * 32 + (lane & 31)) * LD + kq);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < BK; kk += 2) {
-        float af[4], bf[4];
-        const int kq = kk + (lane >> 5);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) af[i] = as[(wm * 128 + i * 32 + (lane & 31)) * LD + kq];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) bf[j] = bs[(wn * 128 + j * 32 + (lane & 31)) * LD + kq];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[j], acc[i][j], 0, 0, 0);
-      }
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) sstore(buf ^ 1);
   }
+}
+
+template <typename T>
+struct SmemBytes;
+template <>
+struct SmemBytes<uint16_t> { static constexpr int value = 2 * 2 * kBM * 64 * 2; };
+template <>
+struct SmemBytes<float> { static constexpr int value = 2 * 2 * kBM * Eng<float>::LD * 4; };
+
+template <typename T, int MODE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void lm_gemm_kernel(const GemmParams p) {
+  __shared__ __attribute__((aligned(16))) char smem_raw[SmemBytes<T>::value];
+  T* smem = reinterpret_cast<T*>(smem_raw);
+  int mb, nb;
+  tile_coords(mb, nb, p.nmb, p.nnb);
+  if (MODE == MODE_FWD && p.store_e == 2 && p.redo_blk[nb] == 0) return;
+  const int m0 = mb * kBM, n0 = nb * kBN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
+  if constexpr (sizeof(T) == 2) mainloop_bf16<MODE>(p, m0, n0, acc, smem);
+  else mainloop_f32<MODE>(p, m0, n0, acc, smem);
 
   // ------------------------------------------------------------------ epilogues
   if constexpr (MODE == MODE_FWD) {
