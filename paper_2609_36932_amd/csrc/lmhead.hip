@@ -11,15 +11,16 @@
 // Both engines leave the accumulators in the same register layout, so the epilogues are
 // shared.  Work is cut into slabs of whole sequences; per slab:
 //   FWD  C = W . H_slab^T  (rows = vocab, cols = tokens, K = d).  Epilogue: per token,
-//        the block's max and sum exp(z - max) over its 256 vocab rows (in-lane over 64
-//        values, then one lane swap and one LDS exchange), the sampled token's logit,
-//        and E = exp(z - s_t) stored twice: E1[t][v] and E2[v][t].
-//   merge   partials -> lse, logp, row max; rows whose exp(z) would leave float range get
-//           s_t = max_t and their token block is evaluated again (rare).
+//        the block's max and sum exp(z - s_t) over its 256 vocab rows (in-lane over 64
+//        values, then one lane swap and one LDS exchange), the sampled token's logit, and
+//        E1[t][v] = exp(z - s_t) (s_t = 0 unless exp(z) would leave float range).
+//   merge   partials -> lse, logp, row max; rows whose max is too far from s_t get
+//           s_t = max_t and their token block is evaluated again (rare), then merge again.
 //   loss    g_t and c_t = g_t exp(s_t - lse_t) per token (one block per sequence).
 //   DH   C = E1 . W^T  (rows = tokens, cols = d, K = vocab):
 //        dH[t] = g_t W[y_t] - c_t C[t].
-//   DW   C = E2 . Bd^T with Bd[n][t] = c_t H[t][n]  (rows = vocab, cols = d, K = tokens):
+//   DW   C = E1^T . Bd^T with Bd[n][t] = c_t H[t][n]  (rows = vocab, cols = d, K = tokens;
+//        E1 is read K-major through transposing LDS reads):
 //        dW[v] (+)= -C[v] + sum_{t in slab, y_t = v} g_t H[t].
 // Nothing of size [T, V] exists; the slab buffers hold [slab, V].
 #include <algorithm>
@@ -75,11 +76,10 @@ struct GemmParams {
   float* zlab;              // [slab]
   const int32_t* yslab;     // [slab] label of each slab token (-1: invalid)
   const float* shift;       // [slab] s_t (nullable = 0)
-  void* E1;                 // [ldE1 rows][V_pad]   E1[t][v]
-  void* E2;                 // [V_pad][Tc_pad]     E2[v][t]
-  int64_t ldE1, ldE2;
+  void* E1;                 // [slab rows][ldE1 = V_pad]   E1[t][v] = exp(z[t][v] - s_t)
+  int64_t ldE1;
   int32_t Vreal;
-  int32_t store_e;          // 0: partials only, 1: partials + E, 2: E only (redo pass)
+  int32_t store_e;          // 0: partials only, 1: partials + E, 2: same for redo blocks
   const int32_t* redo_blk;  // [nnb] token blocks to evaluate again (store_e == 2)
   // ---- DH epilogue
   void* dH;                 // [.., d] at slab offset
@@ -145,16 +145,24 @@ __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 // bf16 main loop.  LDS holds two stages of a 256 x 64 A tile and a 256 x 64 B tile
 // (32 KB each), written by direct global->LDS loads (global_load_lds_dwordx4): one load
-// instruction moves 8 rows x 128 B, lane l writing the 16-byte slot l of that 1 KB.  Row r
-// keeps its k-chunk c (8 bf16) in slot c ^ ((r >> 1) & 7): the LDS serves a 16-byte-per-lane
-// read 16 lanes (256 B, 64 banks) at a time, and rows r..r+15 of a fragment then land on 16
-// distinct 16-byte bank groups (two rows share each 256 B line, parity picks the half).
-// Tile kt+2 is fetched while tile kt is multiplied; fragments of k-step kk+1 are read while
-// the MFMAs of k-step kk run.
-template <int MODE>
+// instruction moves 1 KB, lane l writing its 16-byte slot l.  Tile kt+2 is fetched while
+// tile kt is multiplied; fragments of k-step kk+1 are read while the MFMAs of k-step kk run.
+//
+// K-contiguous operand (rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
+// c ^ ((r >> 1) & 7).  The LDS serves a 16-byte-per-lane read 16 lanes (256 B, 64 banks) at a
+// time, and rows r..r+15 of a fragment then land on 16 distinct 16-byte bank groups.
+//
+// K-major A (A_KMAJOR: A[m][k] stored at k * lda + m, i.e. the logits-exp tile E[t][v] read
+// as E^T for dW): the tile is 64 rows of k x 256 m (512 B), row k keeping its m-chunk c in
+// slot c ^ ((k & 3) << 2).  Fragments come from ds_read_b64_tr_b16: inside each 16-lane group,
+// source lane j reads 4 consecutive m of row kbase + j/4 at m = mbase + 4 (j % 4), and lane i
+// receives A[mbase + i][kbase .. kbase + 3] -- 4 consecutive k of one row m, as the MFMA wants.
+template <int MODE, bool A_KMAJOR>
 __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n0,
                                               f32x16_t (&acc)[4][4], uint16_t* smem) {
   constexpr int BK = 64;
@@ -172,8 +180,16 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int r = wave * 64 + j * 8 + lrow;
-    const int ra = min(m0 + r, p.M - 1);   // rows past the edge load a valid row; their
-    arow[j] = int64_t(ra) * p.lda;         // results are never stored
+    if (!A_KMAJOR) {
+      const int ra = min(m0 + r, p.M - 1);  // rows past the edge load a valid row; their
+      arow[j] = int64_t(ra) * p.lda;        // results are never stored
+    } else {
+      // K-major A: instruction j moves rows k = 2 (8 wave + j) + (lane >> 5) of the tile,
+      // 32 slots of 16 B each; slot (lane & 31) holds m-chunk (lane & 31) ^ ((k & 3) << 2)
+      const int kr = 2 * (wave * 8 + j) + (lane >> 5);
+      const int c = (lane & 31) ^ ((kr & 3) << 2);
+      arow[j] = int64_t(kr) * p.lda + m0 + c * 8;
+    }
     const int rb = min(n0 + r, p.N - 1);
     int64_t br = rb;
     if (MODE == MODE_FWD) {
@@ -184,7 +200,7 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   }
   const int K = p.K;
   const int nk = (K + BK - 1) / BK;
-  const bool ktail = (K % BK) != 0;
+  const bool ktail = (K % BK) != 0;  // never true for K-major A (K is padded to 256)
   auto issue = [&](int kt, int stage) {
     // clamp the chunk so a partial last tile never reads past the end of a row
     const int kc0 = min(kt * BK + gch[0] * 8, K - 8);
@@ -194,7 +210,12 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int kc = (j & 1) ? kc1 : kc0;
-      __builtin_amdgcn_global_load_lds(Ag + arow[j] + kc, (lds_void_t*)(sa + j * 8 * BK), 16, 0, 0);
+      if (A_KMAJOR)
+        __builtin_amdgcn_global_load_lds(Ag + arow[j] + int64_t(kt) * BK * p.lda,
+                                         (lds_void_t*)(sa + j * 8 * BK), 16, 0, 0);
+      else
+        __builtin_amdgcn_global_load_lds(Ag + arow[j] + kc, (lds_void_t*)(sa + j * 8 * BK), 16,
+                                         0, 0);
       __builtin_amdgcn_global_load_lds(Bg + brow[j] + kc, (lds_void_t*)(sb + j * 8 * BK), 16, 0, 0);
     }
   };
@@ -209,13 +230,41 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     }
   };
   const int sw = (lane >> 1) & 7;  // ((row >> 1) & 7) of the fragment rows this lane reads
+  // K-major A fragment source: group g = lane / 16, i = lane % 16 reads row
+  // k = 8 (g / 2) + 4 s + i / 4 (s = first / second half of the 8 k), m = 16 (g % 2) + 4 (i % 4)
+  const int tg = lane >> 4, ti = lane & 15;
+  const int tr_k = 8 * (tg >> 1) + (ti >> 2);
+  const int tr_m = 16 * (tg & 1) + 4 * (ti & 3);
   auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[4]) {
     const uint16_t* as = smem + stage * 2 * TILE;
     const uint16_t* bs = as + TILE;
     const int slot = ((kk * 2 + (lane >> 5)) ^ sw) * 8;
+    if (A_KMAJOR) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 32 + (lane & 31)) * BK + slot);
+      for (int i = 0; i < 4; ++i) {
+        const int m = wm * 128 + i * 32 + tr_m;
+        s16x4_t h[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int k = kk * 16 + tr_k + 4 * hh;
+          const int c = (m >> 3) ^ ((k & 3) << 2);
+          // issued as asm: the compiler's wait analysis cannot tell this read from the
+          // in-flight DMA into the other stage and would wait on vmcnt; the step that uses
+          // the result waits explicitly (wait_a)
+          const uint32_t addr = uint32_t(uintptr_t(
+              (const __attribute__((address_space(3))) uint16_t*)(as + k * kBM + c * 8 + (m & 7))));
+          asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(h[hh]) : "v"(addr) : "memory");
+        }
+        const s16x4_t lo = h[0], hi = h[1];
+        typedef short s16x8_t __attribute__((ext_vector_type(8)));
+        const s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        fa[i] = __builtin_bit_cast(bf16x8_t, v);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 32 + (lane & 31)) * BK + slot);
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 128 + j * 32 + (lane & 31)) * BK + slot);
@@ -227,17 +276,28 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
+  constexpr int NREAD = A_KMAJOR ? 4 : 8;  // compiler-visible LDS reads per k-step
+  // K-major A: the asm reads of a step's A fragments must land before its MFMAs; the wait
+  // is tied to the fragment registers so no MFMA using them can move above it
+  // (the B fragments are tied too, so the compiler's own wait for them lands here, before
+  // the next step's reads are issued, and not after them)
+  auto wait_a = [&](bf16x8_t (&fa)[4], bf16x8_t (&fb)[4]) {
+    if (A_KMAJOR)
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(fa[0]), "+v"(fa[1]), "+v"(fa[2]), "+v"(fa[3]), "+v"(fb[0]),
+                     "+v"(fb[1]), "+v"(fb[2]), "+v"(fb[3])::"memory");
+  };
 
   bf16x8_t fa0[4], fb0[4], fa1[4], fb1[4];
-  // pin the order inside a k-step: the 16 MFMAs of this step with the 8 fragment reads of
-  // the next step spread among them (at most 8 LDS reads in flight, so the wait before the
-  // next step's MFMAs is exact, and the last read still has 8 MFMAs to land)
-#define FR_STEP_ORDER()                                  \
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);     \
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);     \
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);     \
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);     \
-  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);     \
+  // pin the order inside a k-step: the 16 MFMAs of this step with the fragment reads of
+  // the next step spread among them (at most one step's reads in flight, so the wait before
+  // the next step's MFMAs is exact, and the last read still has 8 MFMAs to land)
+#define FR_STEP_ORDER()                                          \
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);             \
+  __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);     \
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);             \
+  __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);     \
+  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);             \
   __builtin_amdgcn_sched_barrier(0)
   issue(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -248,12 +308,15 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   int kt = 0;
   for (; kt + 1 < nk; ++kt) {
     const int cur = kt & 1;
+    wait_a(fa0, fb0);
     frags(cur, 1, fa1, fb1);
     mma(fa0, fb0);
     FR_STEP_ORDER();
+    wait_a(fa1, fb1);
     frags(cur, 2, fa0, fb0);
     mma(fa1, fb1);
     FR_STEP_ORDER();
+    wait_a(fa0, fb0);
     frags(cur, 3, fa1, fb1);
     mma(fa0, fb0);
     FR_STEP_ORDER();
@@ -261,28 +324,35 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     if (kt + 2 == nk && ktail) zero_tail(kt + 1, cur ^ 1);
     __syncthreads();                                   // and nobody reads tile kt any more
     if (kt + 2 < nk) issue(kt + 2, cur);
+    wait_a(fa1, fb1);
     frags(cur ^ 1, 0, fa0, fb0);
     mma(fa1, fb1);
     FR_STEP_ORDER();
   }
   {  // last tile
     const int cur = kt & 1;
+    wait_a(fa0, fb0);
     frags(cur, 1, fa1, fb1);
     mma(fa0, fb0);
     FR_STEP_ORDER();
+    wait_a(fa1, fb1);
     frags(cur, 2, fa0, fb0);
     mma(fa1, fb1);
     FR_STEP_ORDER();
+    wait_a(fa0, fb0);
     frags(cur, 3, fa1, fb1);
     mma(fa0, fb0);
     FR_STEP_ORDER();
+    wait_a(fa1, fb1);
     mma(fa1, fb1);
   }
 #undef FR_STEP_ORDER
 }
 
-// float32 main loop (small problems): register-staged loads into padded LDS rows
-template <int MODE>
+// float32 main loop (small problems): register-staged loads into padded LDS rows.  With
+// A_KMAJOR the A operand is stored k-major (A[m][k] at k * lda + m): a thread loads 4
+// consecutive m of one k and scatters them into the tile's rows.
+template <int MODE, bool A_KMAJOR>
 __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0,
                                              f32x16_t (&acc)[4][4], float* smem) {
   using E = Eng<float>;
@@ -298,7 +368,7 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
   const float* arow[LOADS];
   const float* brow[LOADS];
   bool aok[LOADS], bok[LOADS];
-  int kofs[LOADS], srow[LOADS];
+  int kofs[LOADS], srow[LOADS], akk[LOADS], am4[LOADS];
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
     const int v = tid + j * kThreads;
@@ -308,6 +378,8 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
     const int am = m0 + row;
     aok[j] = am < p.M;
     arow[j] = Ag + int64_t(aok[j] ? am : 0) * p.lda;
+    akk[j] = v / (kBM / VEC);         // k-major: k row of the tile
+    am4[j] = (v % (kBM / VEC)) * VEC;  // and 4 consecutive m
     const int bn = n0 + row;
     bok[j] = bn < p.N;
     int64_t br = bok[j] ? bn : 0;
@@ -324,14 +396,26 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
       const int k = k0 + kofs[j];
-      load_vec<float>(arow[j] + k, aok[j] && k < p.K, ra[j]);
+      if (A_KMAJOR) {
+        const int ka = k0 + akk[j];
+        const int mm = m0 + am4[j];
+        load_vec<float>(Ag + int64_t(ka) * p.lda + mm, ka < p.K && mm + VEC <= p.lda, ra[j]);
+      } else {
+        load_vec<float>(arow[j] + k, aok[j] && k < p.K, ra[j]);
+      }
       load_vec<float>(brow[j] + k, bok[j] && k < p.K, rb[j]);
     }
   };
   auto sstore = [&](int buf) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      *reinterpret_cast<u32x4_t*>(As + (buf * kBM + srow[j]) * LD + kofs[j]) = ra[j];
+      if (A_KMAJOR) {
+#pragma unroll
+        for (int q = 0; q < VEC; ++q)
+          As[(buf * kBM + am4[j] + q) * LD + akk[j]] = __uint_as_float(ra[j][q]);
+      } else {
+        *reinterpret_cast<u32x4_t*>(As + (buf * kBM + srow[j]) * LD + kofs[j]) = ra[j];
+      }
       *reinterpret_cast<u32x4_t*>(Bs + (buf * kBM + srow[j]) * LD + kofs[j]) = rb[j];
     }
   };
@@ -385,8 +469,8 @@ void lm_gemm_kernel(const GemmParams p) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
-  if constexpr (sizeof(T) == 2) mainloop_bf16<MODE>(p, m0, n0, acc, smem);
-  else mainloop_f32<MODE>(p, m0, n0, acc, smem);
+  if constexpr (sizeof(T) == 2) mainloop_bf16<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
+  else mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
 
   // ------------------------------------------------------------------ epilogues
   if constexpr (MODE == MODE_FWD) {
@@ -394,6 +478,10 @@ void lm_gemm_kernel(const GemmParams p) {
     float* xmax = reinterpret_cast<float*>(smem);      // [2 wm][256 cols]
     float* xsum = xmax + 2 * kBN;
     const int Vr = p.Vreal;
+    // with a stored exp (store_e != 0) the block's sum is taken relative to the row's shift
+    // s_t, sum_v exp(z - s_t): one exp per logit serves both the sum and the stored E.  The
+    // merge checks that max_t - s_t stays inside (-60, 60) and re-runs rows that do not.
+    const bool rel = p.store_e != 0;
 #pragma unroll
     for (int ni = 0; ni < 4; ++ni) {
       const int cl = acc_col(wn, ni, lane);
@@ -409,62 +497,57 @@ void lm_gemm_kernel(const GemmParams p) {
           const int v = m0 + acc_row(wm, mi, r, lane);
           const float z = acc[mi][ni][r];
           if (v < Vr) mx = fmaxf(mx, z);
-          if (v == y && p.store_e != 2) p.zlab[t] = z;
+          if (v == y) p.zlab[t] = z;
         }
-      if (p.store_e != 2) {
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        if (lane < 32) xmax[wm * kBN + cl] = mx;
-      }
-      if (p.store_e) {
-        // E = exp(z - s_t), zero outside [0, V) x [0, N)
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      if (lane < 32) xmax[wm * kBN + cl] = mx;
+      if (rel) {
+        float ssum = 0.0f;
+        T* e1 = static_cast<T*>(p.E1) + int64_t(t) * p.ldE1;
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
           for (int rg = 0; rg < 4; ++rg) {
-            T e4[4];
+            float e[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              const int r = rg * 4 + q;
-              const int v = m0 + acc_row(wm, mi, r, lane);
-              const float e = (tok_ok && v < Vr) ? __expf(acc[mi][ni][r] - s_t) : 0.0f;
-              e4[q] = from_f32<T>(e);
+              const int v = m0 + acc_row(wm, mi, rg * 4 + q, lane);
+              e[q] = (tok_ok && v < Vr) ? __expf(acc[mi][ni][rg * 4 + q] - s_t) : 0.0f;
+              ssum += e[q];
             }
             const int v0 = m0 + acc_row(wm, mi, rg * 4, lane);
-            T* e1 = static_cast<T*>(p.E1) + int64_t(t) * p.ldE1 + v0;
             if constexpr (sizeof(T) == 2) {
               uint2 pk;
-              pk.x = uint32_t(e4[0]) | (uint32_t(e4[1]) << 16);
-              pk.y = uint32_t(e4[2]) | (uint32_t(e4[3]) << 16);
-              *reinterpret_cast<uint2*>(e1) = pk;
+              pk.x = uint32_t(f32_to_bf16(e[0])) | (uint32_t(f32_to_bf16(e[1])) << 16);
+              pk.y = uint32_t(f32_to_bf16(e[2])) | (uint32_t(f32_to_bf16(e[3])) << 16);
+              *reinterpret_cast<uint2*>(e1 + v0) = pk;
             } else {
-              *reinterpret_cast<float4*>(e1) = make_float4(e4[0], e4[1], e4[2], e4[3]);
-            }
-            if (p.E2) {
-              T* e2 = static_cast<T*>(p.E2) + int64_t(v0) * p.ldE2 + t;
-#pragma unroll
-              for (int q = 0; q < 4; ++q) e2[int64_t(q) * p.ldE2] = e4[q];
+              *reinterpret_cast<float4*>(e1 + v0) = make_float4(e[0], e[1], e[2], e[3]);
             }
           }
+        ssum += __shfl_xor(ssum, 32, 64);
+        if (lane < 32) xsum[wm * kBN + cl] = ssum;
       }
     }
-    if (p.store_e == 2) return;
     __syncthreads();
+    if (!rel) {
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni) {
-      const int cl = acc_col(wn, ni, lane);
-      const float M = fmaxf(xmax[cl], xmax[kBN + cl]);
-      float s = 0.0f;
+      for (int ni = 0; ni < 4; ++ni) {
+        const int cl = acc_col(wn, ni, lane);
+        const float M = fmaxf(xmax[cl], xmax[kBN + cl]);
+        float ssum = 0.0f;
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
+        for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = m0 + acc_row(wm, mi, r, lane);
-          if (v < Vr) s += __expf(acc[mi][ni][r] - M);
-        }
-      s += __shfl_xor(s, 32, 64);
-      if (lane < 32) xsum[wm * kBN + cl] = s;
+          for (int r = 0; r < 16; ++r) {
+            const int v = m0 + acc_row(wm, mi, r, lane);
+            if (v < Vr) ssum += __expf(acc[mi][ni][r] - M);
+          }
+        ssum += __shfl_xor(ssum, 32, 64);
+        if (lane < 32) xsum[wm * kBN + cl] = ssum;
+      }
+      __syncthreads();
     }
-    __syncthreads();
     for (int cl = tid; cl < kBN; cl += kThreads) {
       const int t = n0 + cl;
       if (t < p.N) {
@@ -552,31 +635,63 @@ __global__ void slab_prep_kernel(const int32_t* __restrict__ token_ids,
   if (shift) shift[t] = 0.0f;
 }
 
-// partials -> lse, logp; decide whether a row needs a shifted second pass
-__global__ void merge_kernel(const float* __restrict__ pmax, const float* __restrict__ psum,
-                             int64_t ldp, int32_t nmb, const float* __restrict__ zlab,
-                             const int32_t* __restrict__ yslab, int32_t Tc,
-                             float* __restrict__ lse_out, float* __restrict__ logp_out,
-                             float* __restrict__ shift, int32_t* __restrict__ redo_blk,
-                             int32_t* __restrict__ redo_count) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= Tc) return;
-  float M = -INFINITY;
-  for (int b = 0; b < nmb; ++b) M = fmaxf(M, pmax[int64_t(b) * ldp + t]);
-  float S = 0.0f;
-  for (int b = 0; b < nmb; ++b) S += psum[int64_t(b) * ldp + t] * __expf(pmax[int64_t(b) * ldp + t] - M);
-  const float l = M + __logf(S);
+// partials -> lse, logp.  One block of 256 threads handles 64 tokens; its 4 wavefronts
+// each combine a quarter of the vocabulary blocks, then combine through LDS.
+//   rel == 0: psum = sum exp(z - pmax) per vocab block (log-prob only path)
+//   rel == 1: psum = sum exp(z - s_t); with check != 0 a row whose max is too far from s_t
+//             (exp(z - s_t) could leave float range) gets s_t = max and its token block is
+//             marked for a second evaluation.
+__global__ __launch_bounds__(256) void merge_kernel(
+    const float* __restrict__ pmax, const float* __restrict__ psum, int64_t ldp, int32_t nmb,
+    const float* __restrict__ zlab, const int32_t* __restrict__ yslab, int32_t Tc, int32_t rel,
+    int32_t check, float* __restrict__ lse_out, float* __restrict__ logp_out,
+    float* __restrict__ shift, int32_t* __restrict__ redo_blk, int32_t* __restrict__ redo_count) {
+  __shared__ float sm[4][64], ss[4][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int t = blockIdx.x * 64 + lane;
+  const bool ok = t < Tc;
+  float M = -INFINITY, S = 0.0f;
+  if (ok) {
+    for (int b = wv; b < nmb; b += 4) {
+      const float m = pmax[int64_t(b) * ldp + t];
+      const float x = psum[int64_t(b) * ldp + t];
+      if (rel) {
+        M = fmaxf(M, m);
+        S += x;
+      } else if (m > M) {
+        S = S * __expf(M - m) + x;
+        M = m;
+      } else {
+        S += x * __expf(m - M);
+      }
+    }
+  }
+  sm[wv][lane] = M;
+  ss[wv][lane] = S;
+  __syncthreads();
+  if (wv != 0 || !ok) return;
+  float Mt = sm[0][lane], St = ss[0][lane];
+  for (int w = 1; w < 4; ++w) {
+    const float m = sm[w][lane], x = ss[w][lane];
+    if (rel) {
+      Mt = fmaxf(Mt, m);
+      St += x;
+    } else if (m > Mt) {
+      St = St * __expf(Mt - m) + x;
+      Mt = m;
+    } else if (m > -INFINITY) {
+      St += x * __expf(m - Mt);
+    }
+  }
+  const float s_t = (rel && shift) ? shift[t] : 0.0f;
+  const float l = rel ? s_t + __logf(St) : Mt + __logf(St);
   const int y = yslab[t];
   if (lse_out) lse_out[t] = l;
   if (logp_out) logp_out[t] = y >= 0 ? zlab[t] - l : __int_as_float(0x7fc00000);
-  if (shift) {
-    // E = exp(z - s) must stay finite (z - s <= max - s < 80) and the dominant entries
-    // normal (max - s > -60); s = 0 fails only for extreme logits
-    if (!(M < 80.0f && M > -60.0f)) {
-      shift[t] = M;
-      redo_blk[t / kBN] = 1;
-      atomicAdd(redo_count, 1);
-    }
+  if (rel && check && !(Mt - s_t < 60.0f && Mt - s_t > -60.0f)) {
+    shift[t] = Mt;
+    redo_blk[t / kBN] = 1;
+    atomicAdd(redo_count, 1);
   }
 }
 
@@ -865,8 +980,8 @@ static int token_logprob_impl(const void* hidden, const int32_t* row_index, cons
     p.Vreal = V; p.store_e = 0; p.status = status;
     FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, 2.0 * V * double(Tc) * d, stream)));
     const int32_t nmb = (V + kBM - 1) / kBM;
-    hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream, w.pmax, w.psum,
-                       ch, nmb, w.zlab, w.yslab, Tc, lse ? lse + t0 : (float*)nullptr,
+    hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 64)), dim3(256), 0, stream, w.pmax, w.psum,
+                       ch, nmb, w.zlab, w.yslab, Tc, 0, 0, lse ? lse + t0 : (float*)nullptr,
                        logp + t0, (float*)nullptr, (int32_t*)nullptr, (int32_t*)nullptr);
     FR_LAUNCHED();
   }
@@ -908,7 +1023,7 @@ static SlabPlan plan_slabs(const int64_t* off, int32_t S, int64_t cap) {
 }
 
 struct LossWs {
-  void *WT, *E1, *E2, *Bd;
+  void *WT, *E1, *Bd;
   float *pmax, *psum, *zlab, *shift, *gslab, *cslab, *lse, *logp;
   int32_t *yslab, *redo_blk, *redo_count, *seq_clip, *lab_cnt, *lab_off, *lab_cur, *lab_tok;
   double* seq_loss;
@@ -922,7 +1037,6 @@ static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_
   const bool dh = a.dhidden != nullptr, dw = a.dW != nullptr;
   w.WT = dh ? c.take<char>(size_t(a.d) * Vpad * esz) : nullptr;
   w.E1 = (dh || dw) ? c.take<char>(size_t(tcp) * Vpad * esz) : nullptr;
-  w.E2 = dw ? c.take<char>(size_t(Vpad) * tcp * esz) : nullptr;
   w.Bd = dw ? c.take<char>(size_t(a.d) * tcp * esz) : nullptr;
   w.pmax = c.take<float>(size_t(nmb * tcp));
   w.psum = c.take<float>(size_t(nmb * tcp));
@@ -999,18 +1113,25 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
     p.B = a.hidden; p.ldb = d; p.N = Tc; p.b_rows = a.row_index; p.b_row_base = t0;
     p.K = d;
     p.pmax = w.pmax; p.psum = w.psum; p.ldp = tcp; p.zlab = w.zlab; p.yslab = w.yslab;
-    p.shift = w.shift; p.E1 = w.E1; p.E2 = w.E2; p.ldE1 = Vpad; p.ldE2 = tcp;
+    p.shift = w.shift; p.E1 = w.E1; p.ldE1 = Vpad;
     p.Vreal = V; p.store_e = (dh || dw) ? 1 : 0; p.status = a.status;
     p.redo_blk = w.redo_blk;
     const double f_fwd = 2.0 * double(V) * Tc * d;
     FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, f_fwd, stream)));
-    hipLaunchKernelGGL(merge_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0, stream,
-                       w.pmax, w.psum, tcp, nmb, w.zlab, w.yslab, Tc, w.lse + t0, w.logp + t0,
-                       (dh || dw) ? w.shift : (float*)nullptr, w.redo_blk, w.redo_count);
+    const bool store = dh || dw;
+    hipLaunchKernelGGL(merge_kernel, dim3(nb1d(std::max(Tc, 1), 64)), dim3(256), 0, stream,
+                       w.pmax, w.psum, tcp, nmb, w.zlab, w.yslab, Tc, store ? 1 : 0,
+                       store ? 1 : 0, w.lse + t0, w.logp + t0, store ? w.shift : (float*)nullptr,
+                       w.redo_blk, w.redo_count);
     FR_LAUNCHED();
-    if (dh || dw) {
-      p.store_e = 2;  // token blocks holding a shifted row: store E again
+    if (store) {
+      // token blocks holding a row that needs a shift: evaluate again, then merge again
+      p.store_e = 2;
       FR_TRY((launch_gemm<T, MODE_FWD>(p, -1, 0.0, stream)));
+      hipLaunchKernelGGL(merge_kernel, dim3(nb1d(std::max(Tc, 1), 64)), dim3(256), 0, stream,
+                         w.pmax, w.psum, tcp, nmb, w.zlab, w.yslab, Tc, 1, 0, w.lse + t0,
+                         w.logp + t0, w.shift, w.redo_blk, w.redo_count);
+      FR_LAUNCHED();
     }
     hipLaunchKernelGGL(loss_kernel, dim3(unsigned(s1 - s0)), dim3(256), 0, stream, w.logp,
                        w.lse, a.old_logp, a.ref_logp, a.row_index, a.seq_off, a.adv,
@@ -1053,7 +1174,7 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
                          w.lab_off, V, w.lab_tok);
       FR_LAUNCHED();
       GemmParams q{};
-      q.A = w.E2; q.lda = tcp; q.M = V;
+      q.A = w.E1; q.lda = Vpad; q.M = V;  // read K-major: A[v][t] = E1[t][v]
       q.B = w.Bd; q.ldb = tcp; q.N = d;
       q.K = int32_t(Tr);
       q.dW = a.dW; q.dW_acc = (si > 0 || a.dW_accumulate) ? 1 : 0;
