@@ -91,8 +91,9 @@ def test_workspace_queries(fr):
     a.dhidden_dtype = 0
     n = L.fastrl_policy_loss_workspace_size(ctypes.byref(a))
     Vp = 152064
-    # two [slab, V] bf16 buffers for a 256-token slab, plus the transposed W
-    assert n >= 2 * 256 * Vp * 2 + 3584 * Vp * 2
+    # one [slab, V] bf16 buffer of exp(logits) for a 256-token slab, plus the transposed W
+    assert n >= 256 * Vp * 2 + 3584 * Vp * 2
+    assert n < 2 * 256 * Vp * 2 + 3584 * Vp * 2 + (64 << 20)
 
 
 def test_ars_matches_oracle(fr, golden_dir):
