@@ -1,0 +1,194 @@
+"""GPU parity at the workloads' full sizes (the launch configuration bench.py times).
+
+The oracle cannot evaluate every kept token at the 7B shape (up to 7.5e14 fp64 FLOP), so:
+* pruning, budget and compaction are compared whole (bit-exact);
+* log-probs and dhidden are compared on a seeded sample of kept tokens (GSPO: on whole
+  sampled sequences, whose ratio needs every token), each computed exactly by the oracle;
+* dW, dhidden and the loss are checked through properties that hold at any size:
+  sum_v dW[v] = 0 (relative to the one-hot part), <dW, W> = <dH, H>, and the reported loss
+  equals the loss of the reported log-probs;
+* a slab of whole kept sequences (about 1K tokens) at full V x d runs through the same entry
+  point and is compared element by element, dW included.
+Old/ref log-probs are "current + N(0, 0.05)": exact oracle log-probs for every token the
+oracle checks, a plain-torch fp32 evaluation for the others.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import CONFIGS, make_rollouts, make_dense
+from tests._parity import rel_fro, onehot_parts, LOGP_ATOL, REL
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+N_SAMPLE = 96
+SLAB_TOKENS = 1024
+
+
+@pytest.fixture(scope="module")
+def fr():
+    assert torch.cuda.is_available()
+    import paper_2609_36932_amd as m
+    return m
+
+
+def _torch_logp(H, W, rows, y, chunk=4096):
+    """Plain-torch fp32 log-probs of kept tokens (input synthesis only)."""
+    Wt = W.float().t().contiguous()
+    out = torch.empty(len(rows), dtype=torch.float32, device=H.device)
+    for a in range(0, len(rows), chunk):
+        b = min(len(rows), a + chunk)
+        z = H[rows[a:b]].float() @ Wt
+        out[a:b] = z.gather(1, y[a:b, None])[:, 0] - torch.logsumexp(z, dim=1)
+        del z
+    del Wt
+    return out
+
+
+@pytest.mark.parametrize("c", [2, 3, 4, 5])
+def test_full_config(fr, c):
+    cfg = CONFIGS[c]
+    ro = make_rollouts(cfg)
+    print(f"[fullsize] cfg {c} {cfg.name}: T_total={ro.T_total}", flush=True)
+    H, W = make_dense(cfg, ro.T_total, device=DEV)
+    ref = oracle.hot_path_step(ro.rewards, ro.group_off, ro.token_ids, ro.traj_tok_off,
+                               lmhead=False, keep_ratio=cfg.keep_ratio,
+                               drop_uniform=cfg.drop_uniform)
+    src = ref["tok_src"]
+    koff = ref["kept_tok_off"]
+    T = len(src)
+    S = len(koff) - 1
+    y_all = ro.token_ids[src].astype(np.int64)
+    rng = np.random.default_rng(c)
+    W64 = W.double().cpu().numpy()
+
+    def exact(idx):
+        Hs = H[torch.from_numpy(src[idx]).long().to(DEV)].double().cpu().numpy()
+        lp, lse = oracle.token_logprob(Hs, W64, y_all[idx])
+        return Hs, lp, lse
+
+    # tokens the oracle checks: a seeded sample, or two whole sequences for GSPO
+    if cfg.algo == "gspo":
+        # two short sequences with a nonzero gradient: old = exact + noise makes the sequence
+        # ratio exp(-mean noise), so the clip decision is known before any log-prob
+        L = np.diff(koff)
+        A_k = ref["adv"][ref["kept_traj"]]
+        sr = np.exp([-ro.old_noise[src[koff[i]:koff[i + 1]]].mean() for i in range(S)])
+        live = ((A_k > 0) & (sr <= 1 + cfg.eps_high)) | ((A_k < 0) & (sr >= 1 - cfg.eps_low))
+        cand = [i for i in np.argsort(L, kind="stable") if live[i]]
+        assert len(cand) >= 2
+        sample = np.concatenate([np.arange(koff[i], koff[i + 1]) for i in cand[:2]])
+    else:
+        sample = np.sort(rng.choice(T, size=N_SAMPLE, replace=False))
+    Hs, lp_s, lse_s = exact(sample)
+
+    # old / ref = current + noise; the current log-prob is exact on the checked tokens
+    x = _torch_logp(H, W, torch.from_numpy(src).long().to(DEV),
+                    torch.from_numpy(y_all).to(DEV)).double().cpu().numpy()
+    x[sample] = lp_s
+    old = np.full(ro.T_total, np.nan, dtype=np.float32)
+    refl = np.full(ro.T_total, np.nan, dtype=np.float32)
+    old[src] = (x + ro.old_noise[src]).astype(np.float32)
+    refl[src] = (x + ro.ref_noise[src]).astype(np.float32)
+    # poison pruned rows: the kernels must never read them
+    pruned = np.ones(ro.T_total, dtype=bool)
+    pruned[src] = False
+    H[torch.from_numpy(pruned).to(DEV)] = float("nan")
+
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    out = fr.hot_path_step(t(ro.rewards), t(ro.group_off), t(ro.token_ids), t(ro.traj_tok_off),
+                           H, W, t(old), t(refl) if cfg.beta else None, V=cfg.V,
+                           max_group=int(np.diff(ro.group_off).max()),
+                           max_len=int(ro.lengths.max()), algo=cfg.algo, norm=cfg.norm,
+                           eps_low=cfg.eps_low, eps_high=cfg.eps_high, beta=cfg.beta,
+                           keep_ratio=cfg.keep_ratio, drop_uniform=cfg.drop_uniform, status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0, fr.status_names(st.item())
+    # pruning + compaction: bit-exact
+    assert np.array_equal(out["prune"]["keep_mask"].cpu().numpy(), ref["keep_mask"])
+    assert (out["n_kept"], out["t_kept"]) == (S, T)
+    assert np.array_equal(out["kept_tok_off_host"].numpy(), koff)
+    assert np.array_equal(out["prune"]["tok_src"][:T].cpu().numpy(), src)
+    call = out["call"]
+    logp = call.logp[:T].double().cpu().numpy()
+    assert np.all(np.isfinite(logp))
+    # sampled log-probs
+    err = np.abs(logp[sample] - lp_s).max()
+    assert err < LOGP_ATOL, err
+    # g on the checked tokens from oracle-only inputs; their dhidden rows exactly
+    A = ref["adv"][ref["kept_traj"]]
+    loss_x, g_x, _ = oracle.policy_loss(x, old[src].astype(np.float64),
+                                        refl[src].astype(np.float64) if cfg.beta else None,
+                                        koff, A, algo=cfg.algo, norm=cfg.norm,
+                                        eps_low=cfg.eps_low, eps_high=cfg.eps_high,
+                                        beta=cfg.beta)
+    g_s = g_x[sample]
+    dH_s, _ = oracle.lmhead_backward(Hs, W64, y_all[sample], lse_s, g_s, need_dW=False)
+    dH_gpu = call.dhidden[torch.from_numpy(sample).long().to(DEV)].double().cpu().numpy()
+    e1 = rel_fro(dH_gpu, dH_s)
+    dH1, _ = onehot_parts(Hs, W64, y_all[sample], g_s)
+    e2 = rel_fro(dH_gpu - dH1, dH_s - dH1)
+    assert np.abs(g_s).max() > 0 and e1 < REL and e2 < REL, (e1, e2)
+    # the reported loss is the loss of the reported log-probs
+    loss_gpu = float(call.loss.item())
+    loss_prop, _, _ = oracle.policy_loss(logp, old[src].astype(np.float64),
+                                         refl[src].astype(np.float64) if cfg.beta else None,
+                                         koff, A, algo=cfg.algo, norm=cfg.norm,
+                                         eps_low=cfg.eps_low, eps_high=cfg.eps_high,
+                                         beta=cfg.beta)
+    assert abs(loss_gpu - loss_prop) <= REL * max(abs(loss_prop), 1e-8), (loss_gpu, loss_prop)
+    # dW: the vocabulary sum cancels the one-hot part sum_t g_t H_t; <dW, W> = <dH, H>
+    dW = call.dW
+    Hk = H[torch.from_numpy(src).long().to(DEV)]
+    colsum = dW.double().sum(0)
+    onehot = (torch.from_numpy(g_x).to(DEV)[:, None] * Hk.double()).sum(0)
+    assert colsum.norm().item() <= 1e-2 * onehot.norm().item(), (colsum.norm().item(),
+                                                                 onehot.norm().item())
+    a = (dW.double() * W.double()).sum().item()
+    b = (call.dhidden[:T].double() * Hk.double()).sum().item()
+    assert abs(a - b) <= REL * max(abs(a), abs(b)), (a, b)
+    del dW, Hk, call, out
+    torch.cuda.empty_cache()
+    print(f"[fullsize] cfg {c}: T_kept={T} logp err {err:.2e} dH {e1:.2e}/{e2:.2e} "
+          f"loss {loss_gpu:.6g} ({loss_prop:.6g})", flush=True)
+
+    # ---- a slab of whole kept sequences at full V x d, element by element
+    S2 = int(np.searchsorted(koff, SLAB_TOKENS))
+    S2 = max(1, min(S2, S))
+    T2 = int(koff[S2])
+    idx = np.arange(T2)
+    Hs2, lp2, lse2 = exact(idx)
+    old2 = np.full(ro.T_total, np.nan, dtype=np.float32)
+    ref2 = np.full(ro.T_total, np.nan, dtype=np.float32)
+    old2[src[:T2]] = (lp2 + ro.old_noise[src[:T2]]).astype(np.float32)
+    ref2[src[:T2]] = (lp2 + ro.ref_noise[src[:T2]]).astype(np.float32)
+    A2 = ref["adv"][ref["kept_traj"][:S2]]
+    off2 = koff[:S2 + 1]
+    loss2, g2, info2 = oracle.policy_loss(lp2, old2[src[:T2]].astype(np.float64),
+                                          ref2[src[:T2]].astype(np.float64) if cfg.beta else None,
+                                          off2, A2, algo=cfg.algo, norm=cfg.norm,
+                                          eps_low=cfg.eps_low, eps_high=cfg.eps_high,
+                                          beta=cfg.beta)
+    dH2, dW2 = oracle.lmhead_backward(Hs2, W64, y_all[:T2], lse2, g2)
+    adv_dev = t(ref["adv"].astype(np.float32))
+    call2 = fr.LossCall(H, W, t(ro.token_ids), t(old2), t(off2), torch.from_numpy(off2), adv_dev,
+                        ref_logp=t(ref2) if cfg.beta else None,
+                        seq_index=t(ref["kept_traj"][:S2]), row_index=t(src[:T2].astype(np.int32)),
+                        algo=cfg.algo, norm=cfg.norm, eps_low=cfg.eps_low, eps_high=cfg.eps_high,
+                        beta=cfg.beta, status=st).run()
+    torch.cuda.synchronize()
+    assert st.item() == 0
+    lpg = call2.logp[:T2].double().cpu().numpy()
+    assert np.abs(lpg - lp2).max() < LOGP_ATOL
+    assert abs(call2.loss.item() - loss2) <= REL * max(abs(loss2), 1e-8)
+    assert int(call2.stats[0].item()) == info2["clipped_tokens"]
+    dHg = call2.dhidden[:T2].double().cpu().numpy()
+    dWg = call2.dW.double().cpu().numpy()
+    dH1, dW1 = onehot_parts(Hs2, W64, y_all[:T2], g2)
+    errs = dict(dH=rel_fro(dHg, dH2), dW=rel_fro(dWg, dW2),
+                dH_soft=rel_fro(dHg - dH1, dH2 - dH1), dW_soft=rel_fro(dWg - dW1, dW2 - dW1))
+    print(f"[fullsize] cfg {c} slab of {S2} sequences / {T2} tokens: {errs}", flush=True)
+    for k, v in errs.items():
+        assert v < REL, (k, v)
