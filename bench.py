@@ -40,7 +40,35 @@ def parse():
     ap.add_argument("--slab", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=768)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run one plain device-to-device copy of this many MiB (a "
+                         "known-size reference for the HBM byte counters)")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lmhead_qwen2.5-vl-7b_grpo_hbm_traffic.md")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_36932_amd", "csrc", "lmhead.hip")
+
+
+def kernel_source_hash():
+    import hashlib
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None when
+    there is none or the kernel source changed since the counters were taken."""
+    try:
+        for line in open(TRAFFIC_FILE):
+            if line.startswith("TRAFFIC_JSON "):
+                rec = json.loads(line[len("TRAFFIC_JSON "):])
+                if rec.get("source_hash") != kernel_source_hash():
+                    return None
+                k = rec.get("kernels", {}).get(kernel)
+                return None if k is None else k["bytes_per_launch"]
+    except OSError:
+        return None
+    return None
 
 
 def log(*a):
@@ -148,6 +176,14 @@ def main():
         out = step()
         torch.cuda.synchronize()
         log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        log(f"[bench] copy probe of {args.copy_probe_mib} MiB done")
     fr.profile_reset()
     fr.profile_enable(True)
     torch.cuda.synchronize()
@@ -192,7 +228,8 @@ def main():
                    "kept_tokens_per_step": t_kept, "kept_sequences": out["n_kept"],
                    "total_tokens": ro.T_total, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": ach, "peak": peak,
-                     "unit": "TFLOP/s", "frac": ach / peak, "traffic": None},
+                     "unit": "TFLOP/s", "frac": ach / peak,
+                     "traffic": measured_traffic(dom) if cfg.name == CONFIGS[3].name else None},
         "useful_frac_of_step": useful / peak,
         "kernels": per,
         "gemm_ms_per_step": gemm_ms,

@@ -57,7 +57,7 @@ typedef enum fastrl_status {
   FASTRL_ERR_DTYPE = -4,        /* unknown dtype enum */
   FASTRL_ERR_WORKSPACE = -5,    /* workspace NULL, misaligned or smaller than required */
   FASTRL_ERR_HIP = -6,          /* a HIP runtime call failed (message has the HIP error) */
-  FASTRL_ERR_UNSUPPORTED = -7   /* valid request outside what this build implements */
+  FASTRL_ERR_UNSUPPORTED = -7   /* valid request outside what the library implements */
 } fastrl_status;
 
 /* device status word bits (OR-ed by kernels) */
