@@ -182,7 +182,8 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
  *   (may be NULL): clipped tokens (token objectives) or tokens of clipped sequences (GSPO),
  *   and the count of logit rows re-evaluated with a shift.
  * Limits: d % 8 == 0; S >= 0; every sequence no longer than the slab (slab_tokens, 0 picks
- *   the default of 16384 tokens; a longer sequence raises the slab to its length).
+ *   the default of 32768 tokens; a longer sequence raises the slab to its length).  The
+ *   tokens are spread over ceil(T / slab_tokens) slabs of about equal size.
  * The work runs slab by slab; each slab stores exp(z - s_t) (s_t = 0, or the row max when
  * exp(z) would leave float range) for its tokens in the workspace, so the workspace holds
  * 2 * slab * V * sizeof(dtype) bytes plus small per-token arrays.

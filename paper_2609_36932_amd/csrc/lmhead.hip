@@ -24,6 +24,7 @@
 //        dW[v] (+)= -C[v] + sum_{t in slab, y_t = v} g_t H[t].
 // Nothing of size [T, V] exists; the slab buffers hold [slab, V].
 #include <algorithm>
+#include <cstdlib>
 #include <vector>
 
 #include "common.h"
@@ -276,6 +277,13 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
+  auto mma_half = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4], int h) {
+#pragma unroll
+    for (int i = 2 * h; i < 2 * h + 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
   constexpr int NREAD = A_KMAJOR ? 4 : 8;  // compiler-visible LDS reads per k-step
   // K-major A: the asm reads of a step's A fragments must land before its MFMAs; the wait
   // is tied to the fragment registers so no MFMA using them can move above it
@@ -320,15 +328,35 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     frags(cur, 3, fa1, fb1);
     mma(fa0, fb0);
     FR_STEP_ORDER();
+    // last k-step: half of its MFMAs cover the barrier; the other half cover the next
+    // tile's load issue and the first fragment reads of tile kt+1
+    wait_a(fa1, fb1);
+    mma_half(fa1, fb1, 0);
+    __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tile kt+1 is in LDS
     if (kt + 2 == nk && ktail) zero_tail(kt + 1, cur ^ 1);
     __syncthreads();                                   // and nobody reads tile kt any more
-    if (kt + 2 < nk) issue(kt + 2, cur);
-    wait_a(fa1, fb1);
+    // the last two iterations re-load tile nk-1 into the free stage (never read): keeps
+    // this block branch-free so the loads can interleave with the MFMAs
+    issue(min(kt + 2, nk - 1), cur);
     frags(cur ^ 1, 0, fa0, fb0);
-    mma(fa1, fb1);
-    FR_STEP_ORDER();
+    mma_half(fa1, fb1, 1);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the re-load above has landed
   {  // last tile
     const int cur = kt & 1;
     wait_a(fa0, fb0);
@@ -1000,23 +1028,39 @@ int run_token_logprob(const void* hidden, const int32_t* row_index, const void* 
 }
 
 // ---------------------------------------------------------------- loss forward/backward
-constexpr int64_t kDefaultSlab = 16384;
+constexpr int64_t kDefaultSlab = 32768;
 
 struct SlabPlan {
   std::vector<int32_t> seq_begin;  // first sequence of each slab; back() == S
   int64_t tc_max = 0;
 };
 
+// Whole sequences per slab; the T tokens go into nslab = ceil(T / cap) slabs of about
+// T / nslab tokens each (each slab ends at the sequence boundary closest to an even share of
+// what is left, never past 1.25 cap unless one sequence is longer), so the last slab is not
+// a small remainder that leaves most of the GPU idle.
 static SlabPlan plan_slabs(const int64_t* off, int32_t S, int64_t cap) {
   SlabPlan pl;
+  const int64_t T = S > 0 ? off[S] - off[0] : 0;
+  const int64_t nslab = std::max<int64_t>(1, (T + cap - 1) / cap);
+  const int64_t hard = cap + cap / 4;
   int32_t i = 0;
+  int64_t k = 0;
   while (i < S) {
     pl.seq_begin.push_back(i);
     const int64_t start = off[i];
-    int32_t j = i + 1;
-    while (j < S && off[j + 1] - start <= cap) ++j;
-    pl.tc_max = std::max<int64_t>(pl.tc_max, off[j] - start);
-    i = j;
+    const int64_t left = nslab - k > 1 ? nslab - k : 1;
+    const int64_t target = (off[S] - start + left - 1) / left;
+    int32_t best = i + 1;
+    if (left == 1) {
+      best = S;
+    } else {
+      for (int32_t j = i + 2; j <= S && off[j] - start <= hard; ++j)
+        if (std::llabs(off[j] - start - target) < std::llabs(off[best] - start - target)) best = j;
+    }
+    pl.tc_max = std::max<int64_t>(pl.tc_max, off[best] - start);
+    i = best;
+    ++k;
   }
   pl.seq_begin.push_back(S);
   return pl;
