@@ -47,17 +47,12 @@ struct Carver {
   size_t size() const { return (off + 255) & ~size_t(255); }
 };
 
-// ---- bf16 helpers (bit-level, round to nearest even) ----------------------------------
+// ---- bf16 helpers ----------------------------------------------------------------------
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __uint_as_float(uint32_t(h) << 16);
 }
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u) {  // inf / nan: keep, quiet the nan
-    return uint16_t((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
-  }
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return uint16_t(u >> 16);
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {  // round to nearest even
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
 __device__ __forceinline__ void set_status(int32_t* status, int32_t bit) {

@@ -510,23 +510,39 @@ void lm_gemm_kernel(const GemmParams p) {
     // s_t, sum_v exp(z - s_t): one exp per logit serves both the sum and the stored E.  The
     // merge checks that max_t - s_t stays inside (-60, 60) and re-runs rows that do not.
     const bool rel = p.store_e != 0;
+    const bool rows_full = m0 + kBM <= Vr;  // every vocab row of this block exists
 #pragma unroll
     for (int ni = 0; ni < 4; ++ni) {
       const int cl = acc_col(wn, ni, lane);
       const int t = n0 + cl;                 // slab token
       const bool tok_ok = t < p.N;
       const int y = tok_ok ? p.yslab[t] : -1;
-      const float s_t = (tok_ok && p.shift) ? p.shift[t] : 0.0f;
+      // columns past the slab store exp(z - inf) = 0
+      const float s_t = tok_ok ? (p.shift ? p.shift[t] : 0.0f) : INFINITY;
       float mx = -INFINITY;
+      if (rows_full) {
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
+        for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = m0 + acc_row(wm, mi, r, lane);
-          const float z = acc[mi][ni][r];
-          if (v < Vr) mx = fmaxf(mx, z);
-          if (v == y) p.zlab[t] = z;
-        }
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[mi][ni][r]);
+      } else {
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            mx = (m0 + acc_row(wm, mi, r, lane) < Vr) ? fmaxf(mx, acc[mi][ni][r]) : mx;
+      }
+      // the sampled token's logit: held by one lane half of one wavefront (rare per column)
+      const int dy = y - m0 - wm * 128;
+      if (dy >= 0 && dy < 128 && ((dy >> 2) & 1) == (lane >> 5)) {
+        float zl = 0.0f;
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            zl = (mi * 32 + (r >> 2) * 8 + (r & 3) == (dy & ~4)) ? acc[mi][ni][r] : zl;
+        p.zlab[t] = zl;
+      }
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       if (lane < 32) xmax[wm * kBN + cl] = mx;
       if (rel) {
@@ -539,15 +555,17 @@ void lm_gemm_kernel(const GemmParams p) {
             float e[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              const int v = m0 + acc_row(wm, mi, rg * 4 + q, lane);
-              e[q] = (tok_ok && v < Vr) ? __expf(acc[mi][ni][rg * 4 + q] - s_t) : 0.0f;
+              e[q] = __expf(acc[mi][ni][rg * 4 + q] - s_t);
+              if (!rows_full && m0 + acc_row(wm, mi, rg * 4 + q, lane) >= Vr) e[q] = 0.0f;
               ssum += e[q];
             }
             const int v0 = m0 + acc_row(wm, mi, rg * 4, lane);
             if constexpr (sizeof(T) == 2) {
+              typedef float f32x2_t __attribute__((ext_vector_type(2)));
+              typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
               uint2 pk;
-              pk.x = uint32_t(f32_to_bf16(e[0])) | (uint32_t(f32_to_bf16(e[1])) << 16);
-              pk.y = uint32_t(f32_to_bf16(e[2])) | (uint32_t(f32_to_bf16(e[3])) << 16);
+              pk.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[0], e[1]}, bf16x2_t));
+              pk.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[2], e[3]}, bf16x2_t));
               *reinterpret_cast<uint2*>(e1 + v0) = pk;
             } else {
               *reinterpret_cast<float4*>(e1 + v0) = make_float4(e[0], e[1], e[2], e[3]);
