@@ -5,9 +5,10 @@
 // of z = H W^T and g = dL/dlogp:  dZ = g (onehot(y) - P),  dH = dZ W,  dW = dZ^T H.
 //
 // One tiled GEMM kernel does the three contractions.  C[m, n] = sum_k A[m, k] B[n, k]
-// with both operands K-contiguous ("NT"), 256 x 256 block tiles, 4 wavefronts of
-// 128 x 128, LDS double buffering, and 32 x 32 MFMA tiles:
-//   bf16: v_mfma_f32_32x32x16_bf16, 64-wide K steps;  f32: v_mfma_f32_32x32x2_f32.
+// with both operands K-contiguous ("NT"), 256 x 256 block tiles, LDS double buffering, and
+// 32 x 32 MFMA tiles:
+//   bf16: 8 wavefronts of 128 x 64, v_mfma_f32_32x32x16_bf16, 64-wide K steps;
+//   f32:  4 wavefronts of 128 x 128, v_mfma_f32_32x32x2_f32.
 // Both engines leave the accumulators in the same register layout, so the epilogues are
 // shared.  Work is cut into slabs of whole sequences; per slab:
 //   FWD  C = W . H_slab^T  (rows = vocab, cols = tokens, K = d).  Epilogue: per token,
@@ -35,7 +36,19 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kBM = 256, kBN = 256, kThreads = 256;
+constexpr int kBM = 256, kBN = 256;
+
+// wavefront geometry of the 256 x 256 block tile
+template <typename T>
+struct Geo;
+template <>
+struct Geo<uint16_t> {  // bf16: 8 wavefronts (two per SIMD) of 128 x 64
+  static constexpr int THREADS = 512, WAVES_N = 4, NI = 2, WPE = 2;
+};
+template <>
+struct Geo<float> {     // f32: 4 wavefronts of 128 x 128
+  static constexpr int THREADS = 256, WAVES_N = 2, NI = 4, WPE = 1;
+};
 
 template <typename T>
 struct Eng;
@@ -141,18 +154,22 @@ __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 __device__ __forceinline__ int acc_row(int wm, int mi, int r, int lane) {
   return wm * 128 + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
 }
+template <typename T>
 __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
-  return wn * 128 + ni * 32 + (lane & 31);
+  return wn * (kBN / Geo<T>::WAVES_N) + ni * 32 + (lane & 31);
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
-// bf16 main loop.  LDS holds two stages of a 256 x 64 A tile and a 256 x 64 B tile
-// (32 KB each), written by direct global->LDS loads (global_load_lds_dwordx4): one load
-// instruction moves 1 KB, lane l writing its 16-byte slot l.  Tile kt+2 is fetched while
-// tile kt is multiplied; fragments of k-step kk+1 are read while the MFMAs of k-step kk run.
+// bf16 main loop.  Eight wavefronts (two per SIMD, so one can issue MFMAs while the
+// other waits on memory) each own a 128 x 64 part of the block tile.  LDS holds two stages
+// of a 256 x 64 A tile and a 256 x 64 B tile (32 KB each), written by direct global->LDS
+// loads (global_load_lds_dwordx4): one load instruction moves 1 KB, lane l writing its
+// 16-byte slot l; each wavefront moves 4 KB of each operand per tile.  Tile kt+1 is in flight
+// while tile kt is multiplied; fragments of k-step kk+1 are read while the MFMAs of k-step kk
+// run.
 //
 // K-contiguous operand (rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
 // c ^ ((r >> 1) & 7).  The LDS serves a 16-byte-per-lane read 16 lanes (256 B, 64 banks) at a
@@ -165,29 +182,29 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 // receives A[mbase + i][kbase .. kbase + 3] -- 4 consecutive k of one row m, as the MFMA wants.
 template <int MODE, bool A_KMAJOR>
 __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n0,
-                                              f32x16_t (&acc)[4][4], uint16_t* smem) {
+                                              f32x16_t (&acc)[4][2], uint16_t* smem) {
   constexpr int BK = 64;
   constexpr int TILE = kBM * BK;  // elements per operand per stage
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const uint16_t* Ag = static_cast<const uint16_t*>(p.A);
   const uint16_t* Bg = static_cast<const uint16_t*>(p.B);
   const int lrow = lane >> 3;
-  // global k-chunk this lane moves into its slot; rows r0 + lrow with r0 = 8 (8 wave + j),
-  // so ((r >> 1) & 7) = 4 (j & 1) + (lrow >> 1)
+  // global k-chunk this lane moves into its slot; rows r = 32 wave + 8 j + lrow, so
+  // ((r >> 1) & 7) = 4 (j & 1) + (lrow >> 1)
   const int gch[2] = {(lane & 7) ^ (lrow >> 1), (lane & 7) ^ (4 | (lrow >> 1))};
-  int64_t arow[8], brow[8];
+  int64_t arow[4], brow[4];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int r = wave * 64 + j * 8 + lrow;
+  for (int j = 0; j < 4; ++j) {
+    const int r = wave * 32 + j * 8 + lrow;
     if (!A_KMAJOR) {
       const int ra = min(m0 + r, p.M - 1);  // rows past the edge load a valid row; their
       arow[j] = int64_t(ra) * p.lda;        // results are never stored
     } else {
-      // K-major A: instruction j moves rows k = 2 (8 wave + j) + (lane >> 5) of the tile,
+      // K-major A: instruction j moves rows k = 2 (4 wave + j) + (lane >> 5) of the tile,
       // 32 slots of 16 B each; slot (lane & 31) holds m-chunk (lane & 31) ^ ((k & 3) << 2)
-      const int kr = 2 * (wave * 8 + j) + (lane >> 5);
+      const int kr = 2 * (wave * 4 + j) + (lane >> 5);
       const int c = (lane & 31) ^ ((kr & 3) << 2);
       arow[j] = int64_t(kr) * p.lda + m0 + c * 8;
     }
@@ -206,10 +223,10 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     // clamp the chunk so a partial last tile never reads past the end of a row
     const int kc0 = min(kt * BK + gch[0] * 8, K - 8);
     const int kc1 = min(kt * BK + gch[1] * 8, K - 8);
-    uint16_t* sa = smem + stage * 2 * TILE + wave * 64 * BK;
+    uint16_t* sa = smem + stage * 2 * TILE + wave * 32 * BK;
     uint16_t* sb = sa + TILE;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < 4; ++j) {
       const int kc = (j & 1) ? kc1 : kc0;
       if (A_KMAJOR)
         __builtin_amdgcn_global_load_lds(Ag + arow[j] + int64_t(kt) * BK * p.lda,
@@ -221,9 +238,9 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     }
   };
   auto zero_tail = [&](int kt, int stage) {  // this lane's slots past K in tile kt
-    uint16_t* sa = smem + stage * 2 * TILE + wave * 64 * BK + lane * 8;
+    uint16_t* sa = smem + stage * 2 * TILE + wave * 32 * BK + lane * 8;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < 4; ++j) {
       if (kt * BK + gch[j & 1] * 8 >= K) {
         *reinterpret_cast<u32x4_t*>(sa + j * 8 * BK) = u32x4_t{0u, 0u, 0u, 0u};
         *reinterpret_cast<u32x4_t*>(sa + TILE + j * 8 * BK) = u32x4_t{0u, 0u, 0u, 0u};
@@ -236,7 +253,7 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   const int tg = lane >> 4, ti = lane & 15;
   const int tr_k = 8 * (tg >> 1) + (ti >> 2);
   const int tr_m = 16 * (tg & 1) + 4 * (ti & 3);
-  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[4]) {
+  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2]) {
     const uint16_t* as = smem + stage * 2 * TILE;
     const uint16_t* bs = as + TILE;
     const int slot = ((kk * 2 + (lane >> 5)) ^ sw) * 8;
@@ -267,45 +284,45 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
         fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 32 + (lane & 31)) * BK + slot);
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 128 + j * 32 + (lane & 31)) * BK + slot);
+    for (int j = 0; j < 2; ++j)
+      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 64 + j * 32 + (lane & 31)) * BK + slot);
   };
-  auto mma = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4]) {
+  auto mma = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[2]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
-  auto mma_half = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4], int h) {
+  auto mma_half = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[2], int h) {
 #pragma unroll
     for (int i = 2 * h; i < 2 * h + 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
-  constexpr int NREAD = A_KMAJOR ? 4 : 8;  // compiler-visible LDS reads per k-step
+  constexpr int NREAD = A_KMAJOR ? 2 : 6;  // compiler-visible LDS reads per k-step
   // K-major A: the asm reads of a step's A fragments must land before its MFMAs; the wait
   // is tied to the fragment registers so no MFMA using them can move above it
   // (the B fragments are tied too, so the compiler's own wait for them lands here, before
   // the next step's reads are issued, and not after them)
-  auto wait_a = [&](bf16x8_t (&fa)[4], bf16x8_t (&fb)[4]) {
+  auto wait_a = [&](bf16x8_t (&fa)[4], bf16x8_t (&fb)[2]) {
     if (A_KMAJOR)
       asm volatile("s_waitcnt lgkmcnt(0)"
                    : "+v"(fa[0]), "+v"(fa[1]), "+v"(fa[2]), "+v"(fa[3]), "+v"(fb[0]),
-                     "+v"(fb[1]), "+v"(fb[2]), "+v"(fb[3])::"memory");
+                     "+v"(fb[1])::"memory");
   };
 
-  bf16x8_t fa0[4], fb0[4], fa1[4], fb1[4];
-  // pin the order inside a k-step: the 16 MFMAs of this step with the fragment reads of
+  bf16x8_t fa0[4], fb0[2], fa1[4], fb1[2];
+  // pin the order inside a k-step: the 8 MFMAs of this step with the fragment reads of
   // the next step spread among them (at most one step's reads in flight, so the wait before
-  // the next step's MFMAs is exact, and the last read still has 8 MFMAs to land)
-#define FR_STEP_ORDER()                                          \
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);             \
-  __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);     \
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);             \
-  __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);     \
-  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);             \
+  // the next step's MFMAs is exact, and the last read still has 4 MFMAs to land)
+#define FR_STEP_ORDER()                                              \
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                 \
+  __builtin_amdgcn_sched_group_barrier(0x100, (NREAD + 1) / 2, 0);   \
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                 \
+  __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);         \
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                 \
   __builtin_amdgcn_sched_barrier(0)
   issue(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -346,14 +363,9 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, (NREAD + 1) / 2, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the re-load above has landed
@@ -386,7 +398,7 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
   using E = Eng<float>;
   constexpr int BK = E::BK, LD = E::LD, VEC = E::VEC;
   constexpr int VPR = BK / VEC;
-  constexpr int LOADS = kBM * VPR / kThreads;
+  constexpr int LOADS = kBM * VPR / Geo<float>::THREADS;
   float* As = smem;
   float* Bs = smem + 2 * kBM * LD;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -399,7 +411,7 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
   int kofs[LOADS], srow[LOADS], akk[LOADS], am4[LOADS];
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
-    const int v = tid + j * kThreads;
+    const int v = tid + j * Geo<float>::THREADS;
     const int row = v / VPR;
     kofs[j] = (v % VPR) * VEC;
     srow[j] = row;
@@ -481,7 +493,8 @@ template <>
 struct SmemBytes<float> { static constexpr int value = 2 * 2 * kBM * Eng<float>::LD * 4; };
 
 template <typename T, int MODE>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(Geo<T>::THREADS)
+__attribute__((amdgpu_waves_per_eu(Geo<T>::WPE, Geo<T>::WPE)))
 void lm_gemm_kernel(const GemmParams p) {
   __shared__ __attribute__((aligned(16))) char smem_raw[SmemBytes<T>::value];
   T* smem = reinterpret_cast<T*>(smem_raw);
@@ -489,14 +502,15 @@ void lm_gemm_kernel(const GemmParams p) {
   tile_coords(mb, nb, p.nmb, p.nnb);
   if (MODE == MODE_FWD && p.store_e == 2 && p.redo_blk[nb] == 0) return;
   const int m0 = mb * kBM, n0 = nb * kBN;
+  constexpr int NI = Geo<T>::NI, NT = Geo<T>::THREADS;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / Geo<T>::WAVES_N, wn = wave % Geo<T>::WAVES_N;
 
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][NI];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
+    for (int j = 0; j < NI; ++j) acc[i][j] = f32x16_t{};
   if constexpr (sizeof(T) == 2) mainloop_bf16<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
   else mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
 
@@ -512,8 +526,8 @@ void lm_gemm_kernel(const GemmParams p) {
     const bool rel = p.store_e != 0;
     const bool rows_full = m0 + kBM <= Vr;  // every vocab row of this block exists
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni) {
-      const int cl = acc_col(wn, ni, lane);
+    for (int ni = 0; ni < NI; ++ni) {
+      const int cl = acc_col<T>(wn, ni, lane);
       const int t = n0 + cl;                 // slab token
       const bool tok_ok = t < p.N;
       const int y = tok_ok ? p.yslab[t] : -1;
@@ -578,8 +592,8 @@ void lm_gemm_kernel(const GemmParams p) {
     __syncthreads();
     if (!rel) {
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const int cl = acc_col(wn, ni, lane);
+      for (int ni = 0; ni < NI; ++ni) {
+        const int cl = acc_col<T>(wn, ni, lane);
         const float M = fmaxf(xmax[cl], xmax[kBN + cl]);
         float ssum = 0.0f;
 #pragma unroll
@@ -594,7 +608,7 @@ void lm_gemm_kernel(const GemmParams p) {
       }
       __syncthreads();
     }
-    for (int cl = tid; cl < kBN; cl += kThreads) {
+    for (int cl = tid; cl < kBN; cl += NT) {
       const int t = n0 + cl;
       if (t < p.N) {
         p.pmax[int64_t(mb) * p.ldp + t] = fmaxf(xmax[cl], xmax[kBN + cl]);
@@ -612,8 +626,8 @@ void lm_gemm_kernel(const GemmParams p) {
           const int y = p.yslab[t];
           const float g = p.gslab[t], c = p.cslab[t];
 #pragma unroll
-          for (int ni = 0; ni < 4; ++ni) {
-            const int n = n0 + acc_col(wn, ni, lane);
+          for (int ni = 0; ni < NI; ++ni) {
+            const int n = n0 + acc_col<T>(wn, ni, lane);
             if (n < p.N) {
               const float wy = y >= 0 ? to_f32<T>(Wg[int64_t(y) * p.d + n]) : 0.0f;
               const float val = g * wy - c * acc[mi][ni][r];
@@ -633,7 +647,7 @@ void lm_gemm_kernel(const GemmParams p) {
         const int v = m0 + acc_row(wm, mi, r, lane);
         if (v < p.M) {
           // onehot part: sum of g_t H[t] over the slab tokens labelled v (index order)
-          float oh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+          float oh[NI] = {};
           const int b0 = p.lab_off[v], b1 = p.lab_off[v + 1];
           for (int e = b0; e < b1; ++e) {
             const int t = p.lab_tok[e];
@@ -642,14 +656,14 @@ void lm_gemm_kernel(const GemmParams p) {
             const float gt = p.gslab[t];
             const T* hrow = Hg + row * p.d;
 #pragma unroll
-            for (int ni = 0; ni < 4; ++ni) {
-              const int n = n0 + acc_col(wn, ni, lane);
+            for (int ni = 0; ni < NI; ++ni) {
+              const int n = n0 + acc_col<T>(wn, ni, lane);
               oh[ni] += n < p.N ? gt * to_f32<T>(hrow[n]) : 0.0f;
             }
           }
 #pragma unroll
-          for (int ni = 0; ni < 4; ++ni) {
-            const int n = n0 + acc_col(wn, ni, lane);
+          for (int ni = 0; ni < NI; ++ni) {
+            const int n = n0 + acc_col<T>(wn, ni, lane);
             if (n < p.N) {
               const int64_t o = int64_t(v) * p.d + n;
               const float prev = p.dW_acc ? p.dW[o] : 0.0f;
@@ -964,7 +978,7 @@ static int launch_gemm(GemmParams p, int kind, double flops, hipStream_t stream)
   const int64_t nblk = int64_t(p.nmb) * p.nnb;
   if (nblk == 0) return FASTRL_OK;
   ProfScope prof(kind, stream, flops);
-  hipLaunchKernelGGL((lm_gemm_kernel<T, MODE>), dim3(unsigned(nblk)), dim3(kThreads), 0,
+  hipLaunchKernelGGL((lm_gemm_kernel<T, MODE>), dim3(unsigned(nblk)), dim3(Geo<T>::THREADS), 0,
                      stream, p);
   FR_LAUNCHED();
   return FASTRL_OK;
