@@ -563,7 +563,8 @@ void lm_gemm_kernel(const GemmParams p) {
         float ssum = 0.0f;
         T* e1 = static_cast<T*>(p.E1) + int64_t(t) * p.ldE1;
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
+        for (int mi = 0; mi < 4; ++mi) {
+          uint32_t pk[8];  // bf16 pairs of the lane's 4-row groups rg = 0..3
 #pragma unroll
           for (int rg = 0; rg < 4; ++rg) {
             float e[4];
@@ -573,18 +574,32 @@ void lm_gemm_kernel(const GemmParams p) {
               if (!rows_full && m0 + acc_row(wm, mi, rg * 4 + q, lane) >= Vr) e[q] = 0.0f;
               ssum += e[q];
             }
-            const int v0 = m0 + acc_row(wm, mi, rg * 4, lane);
             if constexpr (sizeof(T) == 2) {
               typedef float f32x2_t __attribute__((ext_vector_type(2)));
               typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-              uint2 pk;
-              pk.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[0], e[1]}, bf16x2_t));
-              pk.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[2], e[3]}, bf16x2_t));
-              *reinterpret_cast<uint2*>(e1 + v0) = pk;
+              pk[2 * rg] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[0], e[1]}, bf16x2_t));
+              pk[2 * rg + 1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[2], e[3]}, bf16x2_t));
             } else {
+              const int v0 = m0 + acc_row(wm, mi, rg * 4, lane);
               *reinterpret_cast<float4*>(e1 + v0) = make_float4(e[0], e[1], e[2], e[3]);
             }
           }
+          if constexpr (sizeof(T) == 2) {
+            // lane half h holds rows 8 rg + 4 h + 0..3 of this 32-row block; one swap of the
+            // halves' groups (rg 0,1 of the upper half <-> rg 2,3 of the lower half) leaves
+            // lane half h with the 16 consecutive rows 16 h .. 16 h + 15: two 16-byte stores
+            uint32_t P[4] = {pk[0], pk[1], pk[2], pk[3]}, Q[4] = {pk[4], pk[5], pk[6], pk[7]};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              const auto sw2 = __builtin_amdgcn_permlane32_swap(P[k], Q[k], false, false);
+              P[k] = sw2[0];
+              Q[k] = sw2[1];
+            }
+            const int v0 = m0 + wm * 128 + mi * 32 + (lane >> 5) * 16;
+            *reinterpret_cast<uint4*>(e1 + v0) = make_uint4(P[0], P[1], Q[0], Q[1]);
+            *reinterpret_cast<uint4*>(e1 + v0 + 8) = make_uint4(P[2], P[3], Q[2], Q[3]);
+          }
+        }
         ssum += __shfl_xor(ssum, 32, 64);
         if (lane < 32) xsum[wm * kBN + cl] = ssum;
       }
