@@ -119,7 +119,7 @@ __device__ __forceinline__ void tile_coords(int& mb, int& nb, int nmb, int nnb) 
   // consecutive logical tiles on the same XCD (blocks are dealt round-robin to 8 XCDs)
   const int full = (nblk / 8) * 8;
   if (b < full) b = (b % 8) * (full / 8) + b / 8;
-  // grouped order: 8 M-blocks share each N-block sweep
+  // grouped order: 4 M-blocks share each N-block sweep
   constexpr int GROUP = 4;
   const int per_group = GROUP * nnb;
   const int gid = b / per_group;
