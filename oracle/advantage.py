@@ -39,9 +39,15 @@ def group_advantage(rewards, group_off, ddof=1, eps=1e-6, drop_uniform=False):
             valid[q] = 0
             continue
         r = [float(x) for x in r32[a:b]]
-        m = sum(r) / G
+        m = 0.0
+        for x in r:  # index order
+            m += x
+        m = m / G
         if G - ddof > 0:
-            s = math.sqrt(sum((x - m) ** 2 for x in r) / (G - ddof))
+            ss = 0.0
+            for x in r:  # index order
+                ss += (x - m) * (x - m)
+            s = math.sqrt(ss / (G - ddof))
         else:
             s = 0.0
         den = s + eps

@@ -12,7 +12,7 @@ Paper, Sec. 3.2 and Alg. 1 Phase 2:
 
 Readings where the paper is silent or ambiguous:
 * traversal order inside a class: Alg. 1 orders by |A_i| descending, which is
-  constant inside a class, so ties are broken by ascending trajectory index;
+  constant inside a bit-equal class, so ties are broken by ascending trajectory index;
 * tau is a rational tau_num / tau_den and the comparison is done exactly
   (``fractions.Fraction``); theta of two empty n-gram sets is 0, and of one empty
   and one non-empty set is 1 (the definition with |union| > 0);
@@ -26,6 +26,21 @@ Readings where the paper is silent or ambiguous:
   entries are kept.  rho = 0 means pure MDAP.
 * questions marked invalid (DAPO drop of all-equal groups) keep nothing and report
   an MDAP count of 0.
+
+Continuous rewards (appendix on the grounding task; the only change the paper makes
+for continuous rewards is to Eq. grouping): o_i and o_j share an advantage group
+whenever |A_i - A_j| < eps (eps = 1e-4 there).  Readings:
+* that relation is not transitive; the groups are its connected components (single
+  linkage): sort a question's advantages, and a new group starts wherever the gap to
+  the previous sorted value is >= eps;
+* the advantages compared are the float32 values the advantage step outputs, read as
+  exact float64, the gap computed in float64;
+* groups are numbered by their lowest member index, like the bit-equal classes;
+* members of a group now differ in |A|, so Alg. 1's traversal order (|A_i|
+  descending) matters: members are visited by |A| descending, ties by index.  The
+  budget follows the same order: a group's kappa is that of its first visited member,
+  and each round-robin takes the group's next member in visiting order.  With
+  bit-equal classes this is exactly the index order above.
 """
 from fractions import Fraction
 import math
@@ -52,7 +67,7 @@ def theta_below_tau(inter, union, tau_num, tau_den):
 
 
 def greedy_mdap_class(members, sets, tau_num, tau_den):
-    """S'_k: traverse ``members`` (ascending index) and keep o_i unless some kept
+    """S'_k: traverse ``members`` (in the given order) and keep o_i unless some kept
     o_j has theta_ij < tau.  ``sets`` maps member -> n-gram set."""
     kept = []
     for i in members:
@@ -67,16 +82,48 @@ def greedy_mdap_class(members, sets, tau_num, tau_den):
     return kept
 
 
-def class_kappa(rewards_q, cls_q):
-    """kappa per class id: |G * r_k - sum_j r_j| in float64, sum in index order."""
+def continuous_classes(adv_q, eps):
+    """Groups of one question under |A_i - A_j| < eps (connected components, i.e.
+    single linkage over the sorted advantages), numbered by lowest member index.
+    ``adv_q``: the question's float32 advantages."""
+    a = [float(np.float32(x)) for x in adv_q]
+    G = len(a)
+    srt = sorted(range(G), key=lambda i: (a[i], i))
+    comp = [0] * G
+    c = 0
+    for p in range(1, G):
+        if a[srt[p]] - a[srt[p - 1]] >= eps:
+            c += 1
+        comp[srt[p]] = c
+    number = {}
+    cls = []
+    for i in range(G):
+        number.setdefault(comp[i], len(number))
+        cls.append(number[comp[i]])
+    return cls
+
+
+def visit_order(G, adv_q=None):
+    """Traversal order of a question's members: |A| descending, ties by index (Alg. 1);
+    ascending index when no advantages are given."""
+    if adv_q is None:
+        return list(range(G))
+    a = [abs(float(np.float32(x))) for x in adv_q]
+    return sorted(range(G), key=lambda i: (-a[i], i))
+
+
+def class_kappa(rewards_q, cls_q, order=None):
+    """kappa per class id: |G * r_k - sum_j r_j| in float64, sum in index order, r_k
+    the reward of the class's first member in ``order`` (default: index order)."""
     G = len(rewards_q)
     s = 0.0
     for r in rewards_q:
         s += float(r)
     kap = {}
-    for r, c in zip(rewards_q, cls_q):
+    for i in (order if order is not None else range(G)):
+        c = cls_q[i]
         if c not in kap:
-            kap[c] = abs(float(G) * float(r) - s)
+            kap[c] = abs(float(G) * float(rewards_q[i]) - s)
     return kap
 
 
@@ -86,18 +133,20 @@ def budget_size(G, keep_ratio):
     return max(1, min(G, k))
 
 
-def budget_keep(rewards_q, cls_q, mdap_keep_q, keep_ratio):
-    """Apply the keep-ratio budget to one question.  Returns a bool list."""
+def budget_keep(rewards_q, cls_q, mdap_keep_q, keep_ratio, order=None):
+    """Apply the keep-ratio budget to one question.  Returns a bool list.
+    ``order``: the members' visiting order (default: ascending index)."""
     G = len(rewards_q)
-    kap = class_kappa(rewards_q, cls_q)
+    order = list(order) if order is not None else list(range(G))
+    kap = class_kappa(rewards_q, cls_q, order)
     first = {}
     for i, c in enumerate(cls_q):
         first.setdefault(c, i)
-    order = sorted(kap.keys(), key=lambda c: (-kap[c], first[c]))
+    corder = sorted(kap.keys(), key=lambda c: (-kap[c], first[c]))
     priority = []
     for tier in (True, False):
-        lists = [[i for i in range(G) if cls_q[i] == c and bool(mdap_keep_q[i]) == tier]
-                 for c in order]
+        lists = [[i for i in order if cls_q[i] == c and bool(mdap_keep_q[i]) == tier]
+                 for c in corder]
         rnd = 0
         while any(rnd < len(l) for l in lists):
             for l in lists:
@@ -112,26 +161,34 @@ def budget_keep(rewards_q, cls_q, mdap_keep_q, keep_ratio):
 
 
 def prune_prompt(tokens_q, rewards_q, cls_q, ngram_n, tau_num, tau_den, keep_ratio,
-                 valid=True):
-    """One question.  Returns (keep bool[G], mdap_count)."""
+                 valid=True, adv_q=None, group_eps=0.0):
+    """One question.  Returns (keep bool[G], mdap_count, classes used).
+    ``adv_q`` (float32 advantages) sets the visiting order; with ``group_eps`` > 0 the
+    classes are the continuous-reward groups of ``adv_q`` and ``cls_q`` is ignored."""
     G = len(rewards_q)
+    if group_eps > 0:
+        cls_q = continuous_classes(adv_q, group_eps)
     if not valid:
-        return [False] * G, 0
+        return [False] * G, 0, cls_q
+    order = visit_order(G, adv_q)
     sets = [ngram_set(t, ngram_n) for t in tokens_q]
     mdap = [False] * G
     for c in sorted(set(cls_q)):
-        members = [i for i in range(G) if cls_q[i] == c]
+        members = [i for i in order if cls_q[i] == c]
         for i in greedy_mdap_class(members, sets, tau_num, tau_den):
             mdap[i] = True
     count = sum(mdap)
     if keep_ratio > 0:
-        return budget_keep(rewards_q, cls_q, mdap, keep_ratio), count
-    return mdap, count
+        return budget_keep(rewards_q, cls_q, mdap, keep_ratio, order), count, cls_q
+    return mdap, count, cls_q
 
 
 def prune_batch(token_ids, traj_tok_off, rewards, group_off, class_id, group_valid,
-                ngram_n=1, tau_num=4, tau_den=5, keep_ratio=0.0):
-    """Whole batch.  Returns (keep_mask uint8[N], mdap_count int32[Q])."""
+                ngram_n=1, tau_num=4, tau_den=5, keep_ratio=0.0, adv=None, group_eps=0.0,
+                return_classes=False):
+    """Whole batch.  Returns (keep_mask uint8[N], mdap_count int32[Q]) and, with
+    ``return_classes``, the class ids used (int32[N]).  ``adv``: float32[N] advantages
+    (visiting order; required when ``group_eps`` > 0)."""
     tok = np.asarray(token_ids)
     toff = np.asarray(traj_tok_off, dtype=np.int64)
     r32 = np.asarray(rewards, dtype=np.float32)
@@ -140,14 +197,22 @@ def prune_batch(token_ids, traj_tok_off, rewards, group_off, class_id, group_val
     N = int(goff[-1])
     keep = np.zeros(N, dtype=np.uint8)
     counts = np.zeros(Q, dtype=np.int32)
+    used = np.zeros(N, dtype=np.int32)
+    if group_eps > 0 and adv is None:
+        raise ValueError("continuous-reward groups need the advantages")
     for q in range(Q):
         a, b = int(goff[q]), int(goff[q + 1])
         toks = [tok[toff[i]:toff[i + 1]] for i in range(a, b)]
-        k, c = prune_prompt(toks, [float(x) for x in r32[a:b]],
-                            [int(x) for x in class_id[a:b]], ngram_n, tau_num, tau_den,
-                            keep_ratio, bool(group_valid[q]))
+        cq = [int(x) for x in class_id[a:b]] if class_id is not None else [0] * (b - a)
+        k, c, cl = prune_prompt(toks, [float(x) for x in r32[a:b]], cq, ngram_n, tau_num,
+                                tau_den, keep_ratio, bool(group_valid[q]),
+                                None if adv is None else np.asarray(adv[a:b], np.float32),
+                                group_eps)
         keep[a:b] = np.asarray(k, dtype=np.uint8)
         counts[q] = c
+        used[a:b] = np.asarray(cl, dtype=np.int32)
+    if return_classes:
+        return keep, counts, used
     return keep, counts
 
 

@@ -18,15 +18,20 @@ def hot_path_step(rewards, group_off, token_ids, traj_tok_off, *, H=None, W=None
                   old_logp=None, ref_logp=None, algo="grpo",
                   norm="seq_mean_token_mean", eps_low=0.2, eps_high=0.2, beta=0.0,
                   ngram_n=1, tau_num=4, tau_den=5, keep_ratio=0.0,
-                  drop_uniform=False, std_ddof=1, adv_eps=1e-6, lmhead=True):
+                  drop_uniform=False, std_ddof=1, adv_eps=1e-6, group_eps=0.0, lmhead=True):
+    """``group_eps`` > 0: continuous-reward groups |A_i - A_j| < group_eps (appendix on
+    the grounding task) instead of bit-equal reward classes."""
     out = {}
     adv, cls, valid = group_advantage(rewards, group_off, ddof=std_ddof, eps=adv_eps,
                                       drop_uniform=drop_uniform)
     out.update(adv=adv, class_id=cls, group_valid=valid)
-    keep, counts = prune_batch(token_ids, traj_tok_off, rewards, group_off, cls, valid,
-                               ngram_n=ngram_n, tau_num=tau_num, tau_den=tau_den,
-                               keep_ratio=keep_ratio)
-    out.update(keep_mask=keep, mdap_count=counts)
+    # the pruning step sees the float32 advantages the advantage step outputs
+    adv32 = adv.astype(np.float32)
+    keep, counts, used = prune_batch(token_ids, traj_tok_off, rewards, group_off, cls, valid,
+                                     ngram_n=ngram_n, tau_num=tau_num, tau_den=tau_den,
+                                     keep_ratio=keep_ratio, adv=adv32, group_eps=group_eps,
+                                     return_classes=True)
+    out.update(keep_mask=keep, mdap_count=counts, prune_class=used)
     kept, koff, src = compact(keep, traj_tok_off)
     out.update(kept_traj=kept, kept_tok_off=koff, tok_src=src)
     if not lmhead:

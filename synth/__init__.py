@@ -174,6 +174,30 @@ def make_dense(cfg, T_rows, device="cpu", seed=None, d=None, V=None, chunk=1 << 
     return draw(T_rows, h_std, 7), draw(V, w_std, 8)
 
 
+def continuous_rewards(group_off, seed, scale=1.2, near=5e-5):
+    """Continuous rewards shaped like the grounding task's (an IoU-like and a centre-in
+    score): per question a few base values ~ U(0, scale); each rollout repeats a base
+    value exactly (probability 0.4: the same box twice), repeats it up to +-``near``
+    (0.3: a box a few pixels off), or draws a fresh U(0, scale) value.  Exact and near
+    repeats make advantage gaps on both sides of 1e-4.  float32[N]."""
+    rng = _rng(seed, 6)
+    off = np.asarray(group_off, dtype=np.int64)
+    out = np.zeros(int(off[-1]), dtype=np.float32)
+    for q in range(len(off) - 1):
+        a, b = int(off[q]), int(off[q + 1])
+        base = rng.uniform(0.0, scale, size=4)
+        for i in range(a, b):
+            k = int(rng.integers(0, 4))
+            u = rng.uniform()
+            if u < 0.4:
+                out[i] = base[k]
+            elif u < 0.7:
+                out[i] = base[k] + rng.uniform(-near, near)
+            else:
+                out[i] = rng.uniform(0.0, scale)
+    return out
+
+
 def plant_duplicates(ro, p_copy=0.6, p_mutate=0.15, seed=7):
     """Test-only structure: inside each question, overwrite some trajectories with a
     near-copy of the question's first trajectory (each position re-drawn with probability

@@ -50,11 +50,11 @@ def test_golden_mdap_prompt(golden_dir):
         r = np.asarray(p["rewards"], dtype=np.float32)
         _, cls, _ = group_advantage(r, [0, len(r)])
         assert list(cls) == p["class_id"]
-        keep, cnt = prune_prompt(p["tokens"], list(map(float, r)), list(cls), 1, 4, 5, 0.0)
+        keep, cnt, _ = prune_prompt(p["tokens"], list(map(float, r)), list(cls), 1, 4, 5, 0.0)
         assert [int(k) for k in keep] == p["mdap_keep"] and cnt == p["mdap_count"]
         for rho, want in p["budget"].items():
-            keep, cnt = prune_prompt(p["tokens"], list(map(float, r)), list(cls), 1, 4, 5,
-                                     float(rho))
+            keep, cnt, _ = prune_prompt(p["tokens"], list(map(float, r)), list(cls), 1, 4, 5,
+                                        float(rho))
             assert [int(k) for k in keep] == want, (rho, keep)
             assert cnt == p["mdap_count"]
 
