@@ -5,7 +5,7 @@
  * Adaptive Rollout Sampling for GRPO" (arXiv 2609.36932).  One step of the hot path
  * evaluates the kept rollouts only:
  *   fastrl_advantage            group-normalised advantage        (Sec. 3.2, Eq. advantage)
- *   fastrl_prune                MDAP pruning + keep budget + compaction of kept tokens
+ *   fastrl_prune(_ex)           MDAP pruning + keep budget + compaction of kept tokens
  *                                                                 (Sec. 3.2; Alg. 1 Phase 2)
  *   fastrl_token_logprob        LM-head log-prob of the sampled tokens
  *                                                                 (Sec. 3.2, post-pruning evaluation)
@@ -125,7 +125,7 @@ int fastrl_advantage(const float* rewards, const int32_t* group_off, int32_t Q, 
  *   token_ids [T_total] int32 in [0, V);  traj_tok_off [N+1] int64 (trajectory i owns
  *   tokens traj_tok_off[i] .. traj_tok_off[i+1]-1);  rewards [N];  group_off [Q+1];
  *   class_id [N] (from fastrl_advantage);  group_valid [Q] or NULL (all valid).
- *   max_group >= every G_q (<= 1024); max_len >= every trajectory length (<= 16384);
+ *   max_group >= every G_q (<= 256); max_len >= every trajectory length (<= 16384);
  *   V in [1, 2^21); ngram_n in {1, 2, 3}; tau_num >= 0, tau_den > 0; keep_ratio in [0, 1].
  *   Outputs: keep_mask [N] uint8 (0/1), mdap_count [Q] int32, kept_traj [N] (first N_kept
  *   valid), kept_tok_off [N+1] (first N_kept+1 valid), tok_src [T_total] (first T_kept
@@ -141,6 +141,54 @@ int fastrl_prune(const int32_t* token_ids, const int64_t* traj_tok_off, int64_t 
                  int32_t* mdap_count, int32_t* kept_traj, int64_t* kept_tok_off,
                  int32_t* tok_src, int64_t* counts, int32_t* status, void* ws,
                  size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * fastrl_prune_ex -- fastrl_prune with the paper's variants of the advantage partition.
+ *
+ * Fields up to `ws_bytes` mean what the fastrl_prune arguments of the same name mean, and
+ * the workspace is fastrl_prune_workspace_size().  Added:
+ *   adv        [N] float, device, or NULL: the advantages fastrl_advantage wrote.  When
+ *              given, the members of each class are traversed by |A| descending, ties by
+ *              ascending index (Alg. 1 Phase 2 order); inside a class of bit-equal rewards
+ *              that is the ascending index order of fastrl_prune.  The budget follows the
+ *              same order: a class's kappa uses its first visited member's reward, classes
+ *              tie on their lowest member index, and each round takes a class's next member
+ *              in visiting order.
+ *   group_eps  0: classes are class_id (bit-equal rewards, Eq. grouping).  > 0: continuous
+ *              rewards (appendix on the grounding task, eps = 1e-4 there): the classes of a
+ *              question are the connected components of |A_i - A_j| < group_eps over its
+ *              adv values (float32 read as float64, gaps in float64), numbered 0, 1, ... by
+ *              lowest member index.  class_id is then ignored and may be NULL; adv is required.
+ *              Non-finite adv values are treated as 0 and set FASTRL_SB_BAD_REWARD.
+ *   class_out  [N] int32, device, or NULL: the class id each trajectory was pruned under.
+ * fastrl_prune_args_size() returns sizeof(fastrl_prune_args) for binding checks.
+ * Errors as fastrl_prune; group_eps must be finite and >= 0 (FASTRL_ERR_VALUE).
+ * ------------------------------------------------------------------------------------ */
+typedef struct fastrl_prune_args {
+  const int32_t* token_ids;
+  const int64_t* traj_tok_off;
+  int64_t T_total;
+  const float* rewards;
+  const int32_t* group_off;
+  const int32_t* class_id;
+  const uint8_t* group_valid;
+  int32_t Q, N, max_group, max_len, V, ngram_n, tau_num, tau_den;
+  double keep_ratio;
+  uint8_t* keep_mask;
+  int32_t* mdap_count;
+  int32_t* kept_traj;
+  int64_t* kept_tok_off;
+  int32_t* tok_src;
+  int64_t* counts;
+  int32_t* status;
+  void* ws;
+  size_t ws_bytes;
+  const float* adv;
+  double group_eps;
+  int32_t* class_out;
+} fastrl_prune_args;
+size_t fastrl_prune_args_size(void);
+int fastrl_prune_ex(const fastrl_prune_args* args, hipStream_t stream);
 
 /* ------------------------------------------------------------------------------------
  * fastrl_token_logprob -- Sec. 3.2 (post-pruning evaluation): logits of the kept tokens

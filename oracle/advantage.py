@@ -5,7 +5,8 @@ the G rollouts of one question.  Alg. 1 computes it right after the rewards.
 
 Readings where the paper is silent:
 * std uses ``ddof`` (default 1, the sample standard deviation) and ``eps`` is
-  added to the denominator (default 1e-6) so an all-equal group gives A = 0.
+  added to the denominator (default 1e-6) so an all-equal group gives A = 0; eps is
+  a float32 parameter of the library, so the float64 value of float32(eps) is added.
 * Advantage classes (Eq. grouping, S_k = {o_i : A_i = a_k}) are taken as classes of
   equal float32 reward value: within a question A is a strictly increasing function
   of r whenever std > 0, and when std = 0 every A is 0 (one class).  Class ids are
@@ -50,7 +51,7 @@ def group_advantage(rewards, group_off, ddof=1, eps=1e-6, drop_uniform=False):
             s = math.sqrt(ss / (G - ddof))
         else:
             s = 0.0
-        den = s + eps
+        den = s + float(np.float32(eps))
         for i, x in enumerate(r):
             # den == 0 only for an all-equal group with eps == 0: A = 0 (numerator is 0)
             adv[a + i] = (x - m) / den if den > 0 else 0.0

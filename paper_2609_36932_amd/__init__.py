@@ -54,6 +54,18 @@ class LossArgs(ctypes.Structure):
     ]
 
 
+class PruneArgs(ctypes.Structure):
+    _fields_ = [
+        ("token_ids", _vp), ("traj_tok_off", _vp), ("T_total", _i64), ("rewards", _vp),
+        ("group_off", _vp), ("class_id", _vp), ("group_valid", _vp), ("Q", _i32), ("N", _i32),
+        ("max_group", _i32), ("max_len", _i32), ("V", _i32), ("ngram_n", _i32),
+        ("tau_num", _i32), ("tau_den", _i32), ("keep_ratio", _f64), ("keep_mask", _vp),
+        ("mdap_count", _vp), ("kept_traj", _vp), ("kept_tok_off", _vp), ("tok_src", _vp),
+        ("counts", _vp), ("status", _vp), ("ws", _vp), ("ws_bytes", _sz), ("adv", _vp),
+        ("group_eps", _f64), ("class_out", _vp),
+    ]
+
+
 class ARSState(ctypes.Structure):
     _fields_ = [("G", _i32), ("pad_", _i32), ("total_steps", _i64),
                 ("steps_per_epoch", _i64), ("step", _i64), ("G_ref", _f64), ("G_t", _f64),
@@ -69,6 +81,8 @@ _SIGS = {
     "fastrl_prune": (ctypes.c_int, [_vp, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _i32, _i32,
                                     _i32, _i32, _i32, _i32, _i32, _f64, _vp, _vp, _vp, _vp,
                                     _vp, _vp, _vp, _vp, _sz, _vp]),
+    "fastrl_prune_args_size": (_sz, []),
+    "fastrl_prune_ex": (ctypes.c_int, [ctypes.POINTER(PruneArgs), _vp]),
     "fastrl_token_logprob_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
     "fastrl_token_logprob": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i64, _i32, _i32, _vp, _vp,
                                             _vp, _vp, _vp, _sz, _vp]),
@@ -90,6 +104,8 @@ for _name, (_res, _args) in _SIGS.items():
 
 if _lib.fastrl_loss_args_size() != ctypes.sizeof(LossArgs):
     raise ImportError("fastrl_loss_args layout mismatch between libfastrl.so and the binding")
+if _lib.fastrl_prune_args_size() != ctypes.sizeof(PruneArgs):
+    raise ImportError("fastrl_prune_args layout mismatch between libfastrl.so and the binding")
 
 
 class FastRLError(RuntimeError):
@@ -146,8 +162,14 @@ def advantage(rewards, group_off, std_ddof=1, eps=1e-6, drop_uniform=False, stat
 
 
 def prune(token_ids, traj_tok_off, rewards, group_off, class_id, group_valid, *, V,
-          max_group, max_len, ngram_n=1, tau=(4, 5), keep_ratio=0.0, status=None):
-    """MDAP + budget + compaction.  Returns a dict of device tensors (see fastrl.h)."""
+          max_group, max_len, ngram_n=1, tau=(4, 5), keep_ratio=0.0, adv=None, group_eps=0.0,
+          class_out=False, status=None):
+    """MDAP + budget + compaction.  Returns a dict of device tensors (see fastrl.h).
+
+    ``adv`` (the advantages) sets Alg. 1's traversal order (|A| descending); with
+    ``group_eps`` > 0 the classes are the continuous-reward groups |A_i - A_j| < group_eps
+    and ``class_id`` is ignored; ``class_out`` adds the class ids used to the result.  The
+    plain call (no adv, no group_eps, no class_out) goes through ``fastrl_prune``."""
     dev = rewards.device
     Q = group_off.numel() - 1
     N = rewards.numel()
@@ -162,12 +184,29 @@ def prune(token_ids, traj_tok_off, rewards, group_off, class_id, group_valid, *,
     )
     ws_n = _lib.fastrl_prune_workspace_size(Q, N, T_total, max_group, ngram_n)
     ws = _workspace(ws_n, dev)
-    _check(_lib.fastrl_prune(
-        _p(token_ids), _p(traj_tok_off), T_total, _p(rewards), _p(group_off), _p(class_id),
-        _p(group_valid), Q, N, max_group, max_len, V, ngram_n, int(tau[0]), int(tau[1]),
-        float(keep_ratio), _p(out["keep_mask"]), _p(out["mdap_count"]), _p(out["kept_traj"]),
-        _p(out["kept_tok_off"]), _p(out["tok_src"]), _p(out["counts"]), _p(status), _p(ws),
-        ws.numel(), _stream()), "fastrl_prune")
+    if adv is None and not group_eps and not class_out:
+        _check(_lib.fastrl_prune(
+            _p(token_ids), _p(traj_tok_off), T_total, _p(rewards), _p(group_off), _p(class_id),
+            _p(group_valid), Q, N, max_group, max_len, V, ngram_n, int(tau[0]), int(tau[1]),
+            float(keep_ratio), _p(out["keep_mask"]), _p(out["mdap_count"]),
+            _p(out["kept_traj"]), _p(out["kept_tok_off"]), _p(out["tok_src"]),
+            _p(out["counts"]), _p(status), _p(ws), ws.numel(), _stream()), "fastrl_prune")
+        return out
+    if class_out:
+        out["class_id"] = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    a = PruneArgs()
+    a.token_ids, a.traj_tok_off, a.T_total = _p(token_ids), _p(traj_tok_off), T_total
+    a.rewards, a.group_off, a.class_id = _p(rewards), _p(group_off), _p(class_id)
+    a.group_valid, a.Q, a.N, a.max_group, a.max_len = _p(group_valid), Q, N, max_group, max_len
+    a.V, a.ngram_n, a.tau_num, a.tau_den = V, ngram_n, int(tau[0]), int(tau[1])
+    a.keep_ratio = float(keep_ratio)
+    a.keep_mask, a.mdap_count = _p(out["keep_mask"]), _p(out["mdap_count"])
+    a.kept_traj, a.kept_tok_off = _p(out["kept_traj"]), _p(out["kept_tok_off"])
+    a.tok_src, a.counts, a.status = _p(out["tok_src"]), _p(out["counts"]), _p(status)
+    a.ws, a.ws_bytes = _p(ws), ws.numel()
+    a.adv, a.group_eps = _p(adv), float(group_eps)
+    a.class_out = _p(out["class_id"]) if class_out else None
+    _check(_lib.fastrl_prune_ex(ctypes.byref(a), _stream()), "fastrl_prune_ex")
     return out
 
 
@@ -301,13 +340,15 @@ def hot_path_step(rewards, group_off, token_ids, traj_tok_off, hidden, W, old_lo
                   norm="seq_mean_token_mean", eps_low=0.2, eps_high=0.2, beta=0.0,
                   ngram_n=1, tau=(4, 5), keep_ratio=0.0, drop_uniform=False,
                   need_dhidden=True, need_dW=True, slab_tokens=0, status=None,
-                  dhidden_dtype=None):
+                  dhidden_dtype=None, group_eps=0.0):
     """advantage -> prune + compaction -> (one device->host read of the kept counts and
-    offsets) -> loss forward/backward on the kept tokens.  Returns a dict."""
+    offsets) -> loss forward/backward on the kept tokens.  Returns a dict.  ``group_eps``
+    > 0 prunes under continuous-reward groups |A_i - A_j| < group_eps."""
     adv, cls, valid = advantage(rewards, group_off, drop_uniform=drop_uniform, status=status)
     pr = prune(token_ids, traj_tok_off, rewards, group_off, cls, valid, V=V,
                max_group=max_group, max_len=max_len, ngram_n=ngram_n, tau=tau,
-               keep_ratio=keep_ratio, status=status)
+               keep_ratio=keep_ratio, status=status,
+               adv=adv if group_eps else None, group_eps=group_eps)
     counts = pr["counts"].cpu()
     n_kept, t_kept = int(counts[0]), int(counts[1])
     koff_host = pr["kept_tok_off"][:n_kept + 1].cpu()

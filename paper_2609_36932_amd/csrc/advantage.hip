@@ -1,6 +1,9 @@
 // Group-normalised advantage and advantage classes (Sec. 3.2, Eq. advantage and
-// Eq. grouping).  One 64-wide wavefront per question: rewards are summed with
-// wavefront butterfly reductions in float64, then every lane writes its members.
+// Eq. grouping).  One 64-wide wavefront per question: one lane sums the rewards in index
+// order in float64 (correctly rounded operations, no contraction), then every lane writes
+// its members.  The groups are small (G <= 1024), and the fixed order makes the float32
+// advantages exactly reproducible, which the continuous-reward grouping of the pruning
+// step relies on (its decisions compare advantages against a threshold).
 #include "common.h"
 
 namespace fastrl {
@@ -50,24 +53,26 @@ __global__ __launch_bounds__(256) void advantage_kernel(
     if (lane == 0) group_valid[q] = 0;
     return;
   }
-  // mean and std in float64
-  double s1 = 0.0;
+  // mean and std in float64, summed in index order by one lane with explicitly rounded
+  // operations (no contraction), so A is reproducible bit for bit from the rewards
   int bad = 0;
-  for (int i = lane; i < G; i += 64) {
-    float r = rewards[a + i];
-    bad |= !isfinite(r);
-    s1 += double(r);
-  }
+  for (int i = lane; i < G; i += 64) bad |= !isfinite(rewards[a + i]);
   if (wave_sum_i(bad) && lane == 0) set_status(status, FASTRL_SB_BAD_REWARD);
-  const double mean = wave_sum(s1) / double(G);
-  double s2 = 0.0;
-  for (int i = lane; i < G; i += 64) {
-    double dv = double(rewards[a + i]) - mean;
-    s2 += dv * dv;
+  double mean = 0.0, sd = 0.0;
+  if (lane == 0) {
+    double s1 = 0.0;
+    for (int i = 0; i < G; ++i) s1 = __dadd_rn(s1, double(rewards[a + i]));
+    mean = __ddiv_rn(s1, double(G));
+    double s2 = 0.0;
+    for (int i = 0; i < G; ++i) {
+      const double dv = __dsub_rn(double(rewards[a + i]), mean);
+      s2 = __dadd_rn(s2, __dmul_rn(dv, dv));
+    }
+    sd = (G - ddof > 0) ? __dsqrt_rn(__ddiv_rn(s2, double(G - ddof))) : 0.0;
   }
-  s2 = wave_sum(s2);
-  const double sd = (G - ddof > 0) ? sqrt(s2 / double(G - ddof)) : 0.0;
-  const double den = sd + double(eps);
+  mean = __shfl(mean, 0, 64);
+  sd = __shfl(sd, 0, 64);
+  const double den = __dadd_rn(sd, double(eps));
   // classes: first occurrence of each distinct reward value
   int nfirst = 0;
   for (int i = lane; i < G; i += 64) {
@@ -98,8 +103,8 @@ __global__ __launch_bounds__(256) void advantage_kernel(
     int cls = 0;
     for (int k = 0; k < f; ++k) cls += first_flag[wave][k];
     class_id[a + i] = cls;
-    const double num = double(r) - mean;
-    adv[a + i] = (den > 0.0) ? float(num / den) : 0.0f;
+    const double num = __dsub_rn(double(r), mean);
+    adv[a + i] = (den > 0.0) ? float(__ddiv_rn(num, den)) : 0.0f;
   }
   if (lane == 0) group_valid[q] = (drop_uniform && nfirst == 1) ? 0 : 1;
 }

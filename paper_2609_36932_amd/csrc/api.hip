@@ -14,9 +14,10 @@ int launch_advantage(const float*, const int32_t*, int32_t, int32_t, int32_t, fl
                      float*, int32_t*, uint8_t*, int32_t*, hipStream_t);
 size_t prune_workspace(int32_t Q, int32_t N, int64_t T_total, int32_t max_group);
 int launch_prune(const int32_t*, const int64_t*, int64_t, const float*, const int32_t*,
-                 const int32_t*, const uint8_t*, int32_t, int32_t, int32_t, int32_t, int32_t,
-                 int32_t, int32_t, int32_t, double, uint8_t*, int32_t*, int32_t*, int64_t*,
-                 int32_t*, int64_t*, int32_t*, void*, hipStream_t);
+                 const int32_t*, const float*, double, const uint8_t*, int32_t, int32_t,
+                 int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, double, uint8_t*,
+                 int32_t*, int32_t*, int32_t*, int64_t*, int32_t*, int64_t*, int32_t*, void*,
+                 hipStream_t);
 size_t token_logprob_workspace(int64_t T, int32_t d, int32_t V, int32_t dtype);
 int run_token_logprob(const void*, const int32_t*, const void*, int32_t, int64_t, int32_t,
                       int32_t, const int32_t*, float*, float*, int32_t*, void*, hipStream_t);
@@ -97,6 +98,49 @@ size_t fastrl_prune_workspace_size(int32_t Q, int32_t N, int64_t T_total, int32_
   return prune_workspace(Q, N, T_total, max_group);
 }
 
+static int check_and_prune(const fastrl_prune_args& a, hipStream_t stream) {
+  const char* fn = "fastrl_prune";
+  FR_CHECK_ARG(a.Q >= 0 && a.N >= 0 && a.T_total >= 0, FASTRL_ERR_SHAPE,
+               std::string(fn) + ": Q, N, T_total must be >= 0");
+  FR_CHECK_ARG(a.T_total < (int64_t(1) << 31), FASTRL_ERR_SHAPE,
+               std::string(fn) + ": T_total must be < 2^31");
+  FR_CHECK_ARG(a.max_group >= 1 && a.max_group <= 256, FASTRL_ERR_SHAPE,
+               std::string(fn) + ": max_group must be in [1, 256]");
+  FR_CHECK_ARG(a.max_len >= 0 && a.max_len <= 16384, FASTRL_ERR_SHAPE,
+               std::string(fn) + ": max_len must be in [0, 16384]");
+  FR_CHECK_ARG(a.V >= 1 && a.V < (1 << 21), FASTRL_ERR_VALUE,
+               std::string(fn) + ": V must be in [1, 2^21)");
+  FR_CHECK_ARG(a.ngram_n >= 1 && a.ngram_n <= 3, FASTRL_ERR_VALUE,
+               std::string(fn) + ": ngram_n must be 1, 2 or 3");
+  FR_CHECK_ARG(a.tau_num >= 0 && a.tau_den > 0, FASTRL_ERR_VALUE,
+               std::string(fn) + ": need tau_num >= 0 and tau_den > 0");
+  FR_CHECK_ARG(a.keep_ratio >= 0.0 && a.keep_ratio <= 1.0, FASTRL_ERR_VALUE,
+               std::string(fn) + ": keep_ratio must be in [0, 1]");
+  FR_CHECK_ARG(a.group_eps >= 0.0 && std::isfinite(a.group_eps), FASTRL_ERR_VALUE,
+               std::string(fn) + ": group_eps must be finite and >= 0");
+  FR_CHECK_ARG(a.traj_tok_off && a.kept_tok_off && a.counts, FASTRL_ERR_NULL_PTR,
+               std::string(fn) + ": traj_tok_off / kept_tok_off / counts is NULL");
+  FR_CHECK_ARG(a.N == 0 || (a.keep_mask && a.kept_traj && a.rewards), FASTRL_ERR_NULL_PTR,
+               std::string(fn) + ": keep_mask / kept_traj / rewards is NULL");
+  FR_CHECK_ARG(a.N == 0 || a.group_eps > 0.0 || a.class_id, FASTRL_ERR_NULL_PTR,
+               std::string(fn) + ": class_id is NULL (needed unless group_eps > 0)");
+  FR_CHECK_ARG(a.N == 0 || !(a.group_eps > 0.0) || a.adv, FASTRL_ERR_NULL_PTR,
+               std::string(fn) + ": group_eps > 0 needs adv");
+  FR_CHECK_ARG(a.Q == 0 || (a.group_off && a.mdap_count), FASTRL_ERR_NULL_PTR,
+               std::string(fn) + ": group_off / mdap_count is NULL");
+  FR_CHECK_ARG(a.T_total == 0 || (a.token_ids && a.tok_src), FASTRL_ERR_NULL_PTR,
+               std::string(fn) + ": token_ids / tok_src is NULL");
+  const size_t need = prune_workspace(a.Q, a.N, a.T_total, a.max_group);
+  FR_CHECK_ARG(a.ws && aligned256(a.ws) && a.ws_bytes >= need, FASTRL_ERR_WORKSPACE,
+               std::string(fn) + ": workspace missing, misaligned or smaller than " +
+                   std::to_string(need) + " bytes");
+  return launch_prune(a.token_ids, a.traj_tok_off, a.T_total, a.rewards, a.group_off,
+                      a.class_id, a.adv, a.group_eps, a.group_valid, a.Q, a.N, a.max_group,
+                      a.max_len, a.V, a.ngram_n, a.tau_num, a.tau_den, a.keep_ratio,
+                      a.keep_mask, a.mdap_count, a.class_out, a.kept_traj, a.kept_tok_off,
+                      a.tok_src, a.counts, a.status, a.ws, stream);
+}
+
 int fastrl_prune(const int32_t* token_ids, const int64_t* traj_tok_off, int64_t T_total,
                  const float* rewards, const int32_t* group_off, const int32_t* class_id,
                  const uint8_t* group_valid, int32_t Q, int32_t N, int32_t max_group,
@@ -106,37 +150,23 @@ int fastrl_prune(const int32_t* token_ids, const int64_t* traj_tok_off, int64_t 
                  int32_t* tok_src, int64_t* counts, int32_t* status, void* ws,
                  size_t ws_bytes, hipStream_t stream) {
   clear_error();
-  FR_CHECK_ARG(Q >= 0 && N >= 0 && T_total >= 0, FASTRL_ERR_SHAPE,
-               "fastrl_prune: Q, N, T_total must be >= 0");
-  FR_CHECK_ARG(T_total < (int64_t(1) << 31), FASTRL_ERR_SHAPE,
-               "fastrl_prune: T_total must be < 2^31");
-  FR_CHECK_ARG(max_group >= 1 && max_group <= 256, FASTRL_ERR_SHAPE,
-               "fastrl_prune: max_group must be in [1, 256]");
-  FR_CHECK_ARG(max_len >= 0 && max_len <= 16384, FASTRL_ERR_SHAPE,
-               "fastrl_prune: max_len must be in [0, 16384]");
-  FR_CHECK_ARG(V >= 1 && V < (1 << 21), FASTRL_ERR_VALUE, "fastrl_prune: V must be in [1, 2^21)");
-  FR_CHECK_ARG(ngram_n >= 1 && ngram_n <= 3, FASTRL_ERR_VALUE,
-               "fastrl_prune: ngram_n must be 1, 2 or 3");
-  FR_CHECK_ARG(tau_num >= 0 && tau_den > 0, FASTRL_ERR_VALUE,
-               "fastrl_prune: need tau_num >= 0 and tau_den > 0");
-  FR_CHECK_ARG(keep_ratio >= 0.0 && keep_ratio <= 1.0, FASTRL_ERR_VALUE,
-               "fastrl_prune: keep_ratio must be in [0, 1]");
-  FR_CHECK_ARG(traj_tok_off && kept_tok_off && counts, FASTRL_ERR_NULL_PTR,
-               "fastrl_prune: traj_tok_off / kept_tok_off / counts is NULL");
-  FR_CHECK_ARG(N == 0 || (keep_mask && kept_traj && rewards && class_id), FASTRL_ERR_NULL_PTR,
-               "fastrl_prune: keep_mask / kept_traj / rewards / class_id is NULL");
-  FR_CHECK_ARG(Q == 0 || (group_off && mdap_count), FASTRL_ERR_NULL_PTR,
-               "fastrl_prune: group_off / mdap_count is NULL");
-  FR_CHECK_ARG(T_total == 0 || (token_ids && tok_src), FASTRL_ERR_NULL_PTR,
-               "fastrl_prune: token_ids / tok_src is NULL");
-  const size_t need = prune_workspace(Q, N, T_total, max_group);
-  FR_CHECK_ARG(ws && aligned256(ws) && ws_bytes >= need, FASTRL_ERR_WORKSPACE,
-               "fastrl_prune: workspace missing, misaligned or smaller than " +
-                   std::to_string(need) + " bytes");
-  return launch_prune(token_ids, traj_tok_off, T_total, rewards, group_off, class_id,
-                      group_valid, Q, N, max_group, max_len, V, ngram_n, tau_num, tau_den,
-                      keep_ratio, keep_mask, mdap_count, kept_traj, kept_tok_off, tok_src,
-                      counts, status, ws, stream);
+  fastrl_prune_args a{};
+  a.token_ids = token_ids; a.traj_tok_off = traj_tok_off; a.T_total = T_total;
+  a.rewards = rewards; a.group_off = group_off; a.class_id = class_id;
+  a.group_valid = group_valid; a.Q = Q; a.N = N; a.max_group = max_group;
+  a.max_len = max_len; a.V = V; a.ngram_n = ngram_n; a.tau_num = tau_num;
+  a.tau_den = tau_den; a.keep_ratio = keep_ratio; a.keep_mask = keep_mask;
+  a.mdap_count = mdap_count; a.kept_traj = kept_traj; a.kept_tok_off = kept_tok_off;
+  a.tok_src = tok_src; a.counts = counts; a.status = status; a.ws = ws; a.ws_bytes = ws_bytes;
+  return check_and_prune(a, stream);
+}
+
+size_t fastrl_prune_args_size(void) { return sizeof(fastrl_prune_args); }
+
+int fastrl_prune_ex(const fastrl_prune_args* a, hipStream_t stream) {
+  clear_error();
+  FR_CHECK_ARG(a != nullptr, FASTRL_ERR_NULL_PTR, "fastrl_prune_ex: args is NULL");
+  return check_and_prune(*a, stream);
 }
 
 size_t fastrl_token_logprob_workspace_size(int64_t T, int32_t d, int32_t V, int32_t dtype) {

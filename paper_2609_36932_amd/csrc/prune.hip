@@ -5,9 +5,13 @@
 //   K2 pair_conflict one block per question: |N_n(o_i) & N_n(o_j)| for every same-class
 //                   pair by binary search of the shorter key list in the longer one, then
 //                   theta < tau as  tau_den * (|U| - |I|) < tau_num * |U|  in int64.
-//   K3 select       one wavefront per question: the greedy independent set in ascending
-//                   index, then the budget as "keep the K smallest (tier, rank, class
-//                   position) keys" -- the same list a class round-robin produces.
+//   K0 group_eps    (continuous rewards, appendix on the grounding task) one wavefront per
+//                   question: classes = connected components of |A_i - A_j| < eps, from the
+//                   sorted advantages (a new class wherever a gap is >= eps).
+//   K3 select       one wavefront per question: the greedy independent set in visiting
+//                   order (|A| descending, ties by index, when advantages are given; else
+//                   ascending index), then the budget as "keep the K smallest (tier, rank,
+//                   class position) keys" -- the same list a class round-robin produces.
 //   K4 compaction   exclusive scans of kept flags and kept lengths (one block), then a
 //                   coalesced fill of tok_src, one block per kept trajectory.
 #include "common.h"
@@ -107,6 +111,58 @@ __global__ __launch_bounds__(256) void ngram_sort_kernel(
   if (tid == 0) nuniq[i] = base;
 }
 
+// ---------------------------------------------------------------------------- K0
+// Continuous-reward classes of one question: the connected components of the relation
+// |A_i - A_j| < eps over its float32 advantages (read as float64, gaps in float64),
+// numbered by lowest member index.  Sorting by (A, index) puts every component on a run of
+// consecutive positions, and a run ends where the gap to the next value is >= eps.
+__global__ __launch_bounds__(64) void group_eps_kernel(
+    const float* __restrict__ adv, const int32_t* __restrict__ group_off, int32_t N,
+    int32_t max_group, double eps, int32_t* __restrict__ cls_out, int32_t* __restrict__ status) {
+  __shared__ float a[kMaxGroupPrune];
+  __shared__ int32_t sidx[kMaxGroupPrune];   // position -> member
+  __shared__ int32_t comp[kMaxGroupPrune];   // member -> component (in sorted order)
+  __shared__ int32_t label[kMaxGroupPrune];  // component -> class id
+  const int q = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int g0 = group_off[q], g1 = group_off[q + 1];
+  if (g0 < 0 || g1 < g0 || g1 > N || g1 - g0 > max_group) return;  // flagged by K3
+  const int G = g1 - g0;
+  int bad = 0;
+  for (int i = lane; i < G; i += 64) {
+    float v = adv[g0 + i];
+    if (!isfinite(v)) {  // keeps the ranks a permutation
+      bad = 1;
+      v = 0.0f;
+    }
+    a[i] = v;
+  }
+  if (bad) set_status(status, FASTRL_SB_BAD_REWARD);
+  __syncthreads();
+  for (int i = lane; i < G; i += 64) {
+    const float ai = a[i];
+    int r = 0;
+    for (int j = 0; j < G; ++j) r += (a[j] < ai) || (a[j] == ai && j < i);
+    sidx[r] = i;
+  }
+  __syncthreads();
+  if (lane == 0 && G > 0) {
+    int c = 0;
+    comp[sidx[0]] = 0;
+    for (int p = 1; p < G; ++p) {
+      if (__dsub_rn(double(a[sidx[p]]), double(a[sidx[p - 1]])) >= eps) ++c;
+      comp[sidx[p]] = c;
+    }
+    for (int k = 0; k <= c; ++k) label[k] = -1;
+    int next = 0;
+    for (int i = 0; i < G; ++i) {
+      const int k = comp[i];
+      if (label[k] < 0) label[k] = next++;
+      cls_out[g0 + i] = label[k];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------- K2
 __global__ __launch_bounds__(256) void pair_conflict_kernel(
     const int64_t* __restrict__ toff, const int32_t* __restrict__ group_off,
@@ -159,13 +215,18 @@ __global__ __launch_bounds__(256) void pair_conflict_kernel(
 // ---------------------------------------------------------------------------- K3
 __global__ __launch_bounds__(64) void select_kernel(
     const float* __restrict__ rewards, const int32_t* __restrict__ group_off,
-    const int32_t* __restrict__ class_id, const uint8_t* __restrict__ group_valid, int32_t N,
-    int32_t max_group, double keep_ratio, const uint8_t* __restrict__ conflict,
-    uint8_t* __restrict__ keep_mask, int32_t* __restrict__ mdap_count,
+    const int32_t* __restrict__ class_id, const float* __restrict__ adv,
+    const uint8_t* __restrict__ group_valid, int32_t N, int32_t max_group, double keep_ratio,
+    const uint8_t* __restrict__ conflict, uint8_t* __restrict__ keep_mask,
+    int32_t* __restrict__ mdap_count, int32_t* __restrict__ class_out,
     int32_t* __restrict__ status) {
   __shared__ uint8_t mdap[kMaxGroupPrune];
   __shared__ int32_t cls[kMaxGroupPrune];
-  __shared__ int32_t cfirst[kMaxGroupPrune];   // first member of class c
+  __shared__ int32_t vpos[kMaxGroupPrune];     // visiting position of member i
+  __shared__ int32_t ord[kMaxGroupPrune];      // member at visiting position p
+  __shared__ float aabs[kMaxGroupPrune];
+  __shared__ int32_t crep[kMaxGroupPrune];     // first visited member of class c
+  __shared__ int32_t cmin[kMaxGroupPrune];     // lowest member index of class c
   __shared__ double kappa[kMaxGroupPrune];     // kappa of class c
   __shared__ int32_t cpos[kMaxGroupPrune];     // rank of class c in the budget order
   __shared__ int32_t rank[kMaxGroupPrune];     // rank of member i inside its class tier
@@ -188,28 +249,51 @@ __global__ __launch_bounds__(64) void select_kernel(
     }
     return;
   }
+  for (int i = lane; i < G; i += 64) {
+    int c = class_id[g0 + i];
+    if (c < 0 || c >= G) {  // class ids are 0..G-1
+      set_status(status, FASTRL_SB_BAD_INDEX);
+      c = 0;
+    }
+    cls[i] = c;
+    if (class_out) class_out[g0 + i] = c;
+  }
   const bool valid = group_valid ? group_valid[q] != 0 : true;
   if (!valid || G == 0) {
     for (int i = lane; i < G; i += 64) keep_mask[g0 + i] = 0;
     if (lane == 0) mdap_count[q] = 0;
     return;
   }
-  for (int i = lane; i < G; i += 64) {
-    int c = class_id[g0 + i];
-    if (c < 0 || c >= G) {  // class ids come from fastrl_advantage: 0..G-1
-      set_status(status, FASTRL_SB_BAD_INDEX);
-      c = 0;
+  // visiting order: |A| descending, ties by index (Alg. 1); ascending index without A
+  if (adv) {
+    for (int i = lane; i < G; i += 64) {
+      const float v = adv[g0 + i];
+      aabs[i] = isfinite(v) ? fabsf(v) : 0.0f;  // non-finite A was flagged upstream
     }
-    cls[i] = c;
+    __syncthreads();
+    for (int i = lane; i < G; i += 64) {
+      const float ai = aabs[i];
+      int r = 0;
+      for (int j = 0; j < G; ++j) r += (aabs[j] > ai) || (aabs[j] == ai && j < i);
+      vpos[i] = r;
+      ord[r] = i;
+    }
+  } else {
+    for (int i = lane; i < G; i += 64) {
+      vpos[i] = i;
+      ord[i] = i;
+    }
   }
   __syncthreads();
   const uint8_t* cq = conflict + size_t(q) * max_group * max_group;
   if (lane == 0) {
-    // greedy maximal independent set per class, members in ascending index
+    // greedy maximal independent set per class, members in visiting order
     int count = 0;
-    for (int i = 0; i < G; ++i) {
+    for (int p = 0; p < G; ++p) {
+      const int i = ord[p];
       uint8_t keep = 1;
-      for (int j = 0; j < i; ++j) {
+      for (int pj = 0; pj < p; ++pj) {
+        const int j = ord[pj];
         if (mdap[j] && cls[j] == cls[i] && cq[i * max_group + j]) {
           keep = 0;
           break;
@@ -225,27 +309,35 @@ __global__ __launch_bounds__(64) void select_kernel(
     for (int i = lane; i < G; i += 64) keep_mask[g0 + i] = mdap[i];
     return;
   }
-  // budget: kappa_k = |G r_k - sum_j r_j|, sum in index order in float64
-  for (int c = lane; c < G; c += 64) cfirst[c] = -1;
+  // budget: kappa_k = |G r_k - sum_j r_j| (sum in index order, float64; r_k the reward of
+  // the class's first visited member); classes ordered by kappa descending, then by their
+  // lowest member index
+  for (int c = lane; c < G; c += 64) {
+    crep[c] = -1;
+    cmin[c] = -1;
+  }
   __syncthreads();
   if (lane == 0) {
     double s = 0.0;
     for (int j = 0; j < G; ++j) s = __dadd_rn(s, double(rewards[g0 + j]));
-    for (int j = 0; j < G; ++j) {
+    for (int p = 0; p < G; ++p) {
+      const int j = ord[p];
       const int c = cls[j];
-      if (cfirst[c] < 0) {
-        cfirst[c] = j;
+      if (crep[c] < 0) {
+        crep[c] = j;
         kappa[c] = fabs(__dsub_rn(__dmul_rn(double(G), double(rewards[g0 + j])), s));
       }
     }
+    for (int j = 0; j < G; ++j)
+      if (cmin[cls[j]] < 0) cmin[cls[j]] = j;
   }
   __syncthreads();
   for (int c = lane; c < G; c += 64) {
-    if (cfirst[c] < 0) continue;
+    if (crep[c] < 0) continue;
     int pos = 0;
     for (int e = 0; e < G; ++e) {
-      if (cfirst[e] < 0 || e == c) continue;
-      if (kappa[e] > kappa[c] || (kappa[e] == kappa[c] && cfirst[e] < cfirst[c])) ++pos;
+      if (crep[e] < 0 || e == c) continue;
+      if (kappa[e] > kappa[c] || (kappa[e] == kappa[c] && cmin[e] < cmin[c])) ++pos;
     }
     cpos[c] = pos;
   }
@@ -255,7 +347,8 @@ __global__ __launch_bounds__(64) void select_kernel(
   for (int i = lane; i < G; i += 64) {
     const int ti = mdap[i] ? 0 : 1;
     int ri = 0;
-    for (int j = 0; j < i; ++j) ri += (cls[j] == cls[i] && (mdap[j] ? 0 : 1) == ti);
+    for (int j = 0; j < G; ++j)
+      ri += (cls[j] == cls[i] && (mdap[j] ? 0 : 1) == ti && vpos[j] < vpos[i]);
     rank[i] = ri;
   }
   __syncthreads();
@@ -354,22 +447,31 @@ size_t prune_workspace(int32_t Q, int32_t N, int64_t T_total, int32_t max_group)
   c.take<int32_t>(size_t(N + 1));
   c.take<uint8_t>(size_t(Q > 0 ? Q : 1) * max_group * max_group);
   c.take<int32_t>(size_t(N + 1));
+  c.take<int32_t>(size_t(N + 1));
   return c.size();
 }
 
 int launch_prune(const int32_t* token_ids, const int64_t* toff, int64_t T_total,
                  const float* rewards, const int32_t* group_off, const int32_t* class_id,
-                 const uint8_t* group_valid, int32_t Q, int32_t N, int32_t max_group,
-                 int32_t max_len, int32_t V, int32_t ngram_n, int32_t tau_num,
-                 int32_t tau_den, double keep_ratio, uint8_t* keep_mask,
-                 int32_t* mdap_count, int32_t* kept_traj, int64_t* kept_tok_off,
-                 int32_t* tok_src, int64_t* counts, int32_t* status, void* ws,
-                 hipStream_t stream) {
+                 const float* adv, double group_eps, const uint8_t* group_valid, int32_t Q,
+                 int32_t N, int32_t max_group, int32_t max_len, int32_t V, int32_t ngram_n,
+                 int32_t tau_num, int32_t tau_den, double keep_ratio, uint8_t* keep_mask,
+                 int32_t* mdap_count, int32_t* class_out, int32_t* kept_traj,
+                 int64_t* kept_tok_off, int32_t* tok_src, int64_t* counts, int32_t* status,
+                 void* ws, hipStream_t stream) {
   Carver c(ws);
   uint64_t* keys = c.take<uint64_t>(size_t(T_total > 0 ? T_total : 1));
   int32_t* nuniq = c.take<int32_t>(size_t(N + 1));
   uint8_t* conflict = c.take<uint8_t>(size_t(Q > 0 ? Q : 1) * max_group * max_group);
   int32_t* kpos = c.take<int32_t>(size_t(N + 1));
+  int32_t* cls_eps = c.take<int32_t>(size_t(N + 1));
+  const int32_t* cls = class_id;
+  if (group_eps > 0.0 && Q > 0) {
+    hipLaunchKernelGGL(group_eps_kernel, dim3(Q), dim3(64), 0, stream, adv, group_off, N,
+                       max_group, group_eps, cls_eps, status);
+    FR_LAUNCHED();
+    cls = cls_eps;
+  }
   if (N > 0) {
     const int P = next_pow2(max_len > 1 ? max_len : 1);
     const size_t shm = size_t(P) * sizeof(uint64_t);
@@ -382,11 +484,11 @@ int launch_prune(const int32_t* token_ids, const int64_t* toff, int64_t T_total,
   }
   if (Q > 0) {
     hipLaunchKernelGGL(pair_conflict_kernel, dim3(Q), dim3(256), 0, stream, toff, group_off,
-                       class_id, keys, nuniq, N, max_group, tau_num, tau_den, conflict);
+                       cls, keys, nuniq, N, max_group, tau_num, tau_den, conflict);
     FR_LAUNCHED();
-    hipLaunchKernelGGL(select_kernel, dim3(Q), dim3(64), 0, stream, rewards, group_off,
-                       class_id, group_valid, N, max_group, keep_ratio, conflict, keep_mask,
-                       mdap_count, status);
+    hipLaunchKernelGGL(select_kernel, dim3(Q), dim3(64), 0, stream, rewards, group_off, cls,
+                       adv, group_valid, N, max_group, keep_ratio, conflict, keep_mask,
+                       mdap_count, class_out, status);
     FR_LAUNCHED();
   }
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(1024), 0, stream, keep_mask, toff, N,

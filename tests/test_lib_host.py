@@ -39,6 +39,7 @@ def test_exports_every_declared_symbol(fr):
 
 def test_struct_layout(fr):
     assert fr._lib.fastrl_loss_args_size() == ctypes.sizeof(fr.LossArgs)
+    assert fr._lib.fastrl_prune_args_size() == ctypes.sizeof(fr.PruneArgs)
     assert fr._lib.fastrl_version() >= 10000
 
 
@@ -63,6 +64,24 @@ def test_host_validation_errors(fr):
     a = list(args); a[15] = 1.5                   # keep_ratio
     assert L.fastrl_prune(*a) == -3
     assert L.fastrl_prune(*args) == -1            # NULL arrays
+    # fastrl_prune_ex: the same checks plus the continuous-grouping options
+    assert L.fastrl_prune_ex(None, None) == -1
+    pa = fr.PruneArgs()
+    pa.T_total, pa.Q, pa.N, pa.max_group, pa.max_len, pa.V = 10, 2, 16, 8, 64, 1000
+    pa.ngram_n, pa.tau_num, pa.tau_den, pa.keep_ratio = 1, 4, 5, 0.5
+    pa.group_eps = -1e-4
+    assert L.fastrl_prune_ex(ctypes.byref(pa), None) == -3
+    pa.group_eps = float("nan")
+    assert L.fastrl_prune_ex(ctypes.byref(pa), None) == -3
+    dummy = ctypes.c_void_p(256)
+    pa.group_eps = 1e-4
+    pa.traj_tok_off = pa.kept_tok_off = pa.counts = dummy
+    pa.keep_mask = pa.kept_traj = pa.rewards = dummy
+    assert L.fastrl_prune_ex(ctypes.byref(pa), None) == -1       # group_eps > 0 without adv
+    assert b"adv" in L.fastrl_last_error()
+    pa.group_eps = 0.0
+    assert L.fastrl_prune_ex(ctypes.byref(pa), None) == -1       # class_id needed
+    assert b"class_id" in L.fastrl_last_error()
     # dtype / shape checks of the LM-head entry points
     assert L.fastrl_token_logprob(None, None, None, 7, 1, 16, 10, None, None, None, None,
                                   None, 0, None) == -4
