@@ -27,7 +27,7 @@ from .advantage import group_advantage
 from .mdap import (ngram_set, jaccard_counts, theta_below_tau, greedy_mdap_class,
                    budget_keep, prune_prompt, prune_batch, compact, continuous_classes,
                    visit_order)
-from .lmhead import token_logprob, lmhead_backward, logits
+from .lmhead import token_logprob, lmhead_backward, logits, token_entropy
 from .loss import policy_loss, token_weights
 from .ars import ARSController
 from .pipeline import hot_path_step
@@ -36,6 +36,7 @@ __all__ = [
     "group_advantage", "ngram_set", "jaccard_counts", "theta_below_tau",
     "greedy_mdap_class", "budget_keep", "prune_prompt", "prune_batch", "compact",
     "continuous_classes", "visit_order",
-    "token_logprob", "lmhead_backward", "logits", "policy_loss", "token_weights",
+    "token_logprob", "lmhead_backward", "logits", "token_entropy", "policy_loss",
+    "token_weights",
     "ARSController", "hot_path_step",
 ]

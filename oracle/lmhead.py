@@ -15,6 +15,11 @@ is a weighted sum of grad log pi over tokens):
     dZ[t, v] = g[t] * (1[v == y_t] - exp(z[t, v] - lse[t]))
     dH       = dZ @ W,      dW = dZ^T @ H
 
+Policy entropy per token (the statistic the paper follows during training, Sec. 4,
+entropy curves), from its definition over the softmax:
+
+    H[t] = - sum_v p[t, v] log p[t, v],    p[t, v] = exp(z[t, v] - lse[t])
+
 All arithmetic is float64; rows are processed in chunks only to bound memory (rows
 are independent, so chunking changes nothing but the summation order of dW).
 """
@@ -87,4 +92,21 @@ def lmhead_dW_rows(H, W, y, lse, g, vocab_rows, row_chunk=4096):
         dz += (y[a:b, None] == vr[None, :])
         dz *= g[a:b, None]
         out += dz.T @ H[a:b]
+    return out
+
+
+def token_entropy(H, W, row_chunk=64):
+    """Return H float64[T]: -sum_v p log p of each row's softmax (0 log 0 = 0)."""
+    H = _f64(H)
+    W = _f64(W)
+    T = H.shape[0]
+    out = np.empty(T, dtype=np.float64)
+    for a in range(0, T, row_chunk):
+        b = min(T, a + row_chunk)
+        z = H[a:b] @ W.T
+        m = z.max(axis=1)
+        e = np.exp(z - m[:, None])
+        p = e / e.sum(axis=1)[:, None]
+        logp = np.where(p > 0, np.log(np.where(p > 0, p, 1.0)), 0.0)
+        out[a:b] = -(p * logp).sum(axis=1)
     return out
