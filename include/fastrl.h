@@ -228,13 +228,19 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
  *   dhidden [T][d] in dhidden_dtype (NULL: not computed); dW [V][d] float32 (NULL: not
  *   computed), overwritten, or accumulated into when dW_accumulate != 0; stats [2] float
  *   (may be NULL): clipped tokens (token objectives) or tokens of clipped sequences (GSPO),
- *   and the count of logit rows re-evaluated with a shift.
+ *   and the count of logit rows re-evaluated with a shift; stats[0] / T is the clip
+ *   fraction.  entropy [T] float (may be NULL): the policy entropy of each kept token,
+ *   H_t = -sum_v p_v log p_v = lse_t - sum_v p_v z_v (the statistic the paper tracks during
+ *   training, Sec. 4), accumulated in the same pass as the log-sum-exp (one more partial
+ *   sum exp(z - s_t) z per vocabulary block).  entropy_sum [1] float (may be NULL): sum_t H_t
+ *   in float64, fixed order (the mean entropy is entropy_sum / T).
  * Limits: d % 8 == 0; S >= 0; every sequence no longer than the slab (slab_tokens, 0 picks
  *   the default of 32768 tokens; a longer sequence raises the slab to its length).  The
  *   tokens are spread over ceil(T / slab_tokens) slabs of about equal size.
  * The work runs slab by slab; each slab stores exp(z - s_t) (s_t = 0, or the row max when
  * exp(z) would leave float range) for its tokens in the workspace, so the workspace holds
- * 2 * slab * V * sizeof(dtype) bytes plus small per-token arrays.
+ * slab * V_pad * sizeof(dtype) bytes (V_pad = V rounded up to 256), W^T (d * V_pad) when
+ * dhidden is wanted, and small per-token and per-(vocabulary block, token) arrays.
  * ------------------------------------------------------------------------------------ */
 typedef struct fastrl_loss_args {
   const void* hidden;
@@ -269,6 +275,8 @@ typedef struct fastrl_loss_args {
   int32_t* status;
   void* ws;
   size_t ws_bytes;
+  float* entropy;
+  float* entropy_sum;
 } fastrl_loss_args;
 
 /* sizeof(fastrl_loss_args) as compiled into the library (lets bindings check layout). */

@@ -50,7 +50,7 @@ class LossArgs(ctypes.Structure):
         ("eps_high", _f32), ("beta", _f32), ("loss", _vp), ("logp", _vp), ("lse", _vp),
         ("dhidden", _vp), ("dhidden_dtype", _i32), ("dW_accumulate", _i32), ("dW", _vp),
         ("stats", _vp), ("slab_tokens", _i64), ("status", _vp), ("ws", _vp),
-        ("ws_bytes", _sz),
+        ("ws_bytes", _sz), ("entropy", _vp), ("entropy_sum", _vp),
     ]
 
 
@@ -235,7 +235,8 @@ class LossCall:
                  ref_logp=None, seq_index=None, row_index=None, algo="grpo",
                  norm="seq_mean_token_mean", eps_low=0.2, eps_high=0.2, beta=0.0,
                  need_dhidden=True, need_dW=True, dhidden_dtype=None, dW=None,
-                 dW_accumulate=False, slab_tokens=0, status=None, T=None):
+                 dW_accumulate=False, slab_tokens=0, status=None, T=None,
+                 need_entropy=False):
         dev = hidden.device
         dt = _dtype_code(hidden)
         d = hidden.shape[1]
@@ -247,6 +248,10 @@ class LossCall:
         self.stats = torch.zeros(2, dtype=torch.float32, device=dev)
         self.logp = torch.empty(max(T, 1), dtype=torch.float32, device=dev)
         self.lse = torch.empty(max(T, 1), dtype=torch.float32, device=dev)
+        self.entropy = (torch.empty(max(T, 1), dtype=torch.float32, device=dev)
+                        if need_entropy else None)
+        self.entropy_sum = (torch.zeros(1, dtype=torch.float32, device=dev)
+                            if need_entropy else None)
         dhd = torch.float32 if dhidden_dtype is None else dhidden_dtype
         self.dhidden = (torch.empty((max(T, 1), d), dtype=dhd, device=dev)
                         if need_dhidden else None)
@@ -271,6 +276,7 @@ class LossCall:
         a.dW = _p(self.dW)
         a.dW_accumulate = int(bool(dW_accumulate))
         a.stats = _p(self.stats)
+        a.entropy, a.entropy_sum = _p(self.entropy), _p(self.entropy_sum)
         a.slab_tokens = int(slab_tokens)
         a.status = _p(status)
         n = _lib.fastrl_policy_loss_workspace_size(ctypes.byref(a))
@@ -289,7 +295,7 @@ class LossCall:
 
 def policy_loss_fwd_bwd(*args, **kw):
     """One call of fastrl_policy_loss_fwd_bwd; returns the LossCall holding the outputs
-    (loss, logp, lse, dhidden, dW, stats)."""
+    (loss, logp, lse, dhidden, dW, stats, and entropy / entropy_sum with need_entropy)."""
     return LossCall(*args, **kw).run()
 
 

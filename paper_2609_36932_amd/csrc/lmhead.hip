@@ -86,6 +86,7 @@ struct GemmParams {
   // ---- FWD epilogue
   float* pmax;              // [nmb][ldp]
   float* psum;              // [nmb][ldp]
+  float* psz;               // [nmb][ldp] or NULL: sum of exp(z - ref) * z (entropy)
   int64_t ldp;
   float* zlab;              // [slab]
   const int32_t* yslab;     // [slab] label of each slab token (-1: invalid)
@@ -519,6 +520,7 @@ void lm_gemm_kernel(const GemmParams p) {
     __syncthreads();  // LDS operand buffers are reused for the cross-wave exchange
     float* xmax = reinterpret_cast<float*>(smem);      // [2 wm][256 cols]
     float* xsum = xmax + 2 * kBN;
+    float* xsz = xsum + 2 * kBN;
     const int Vr = p.Vreal;
     // with a stored exp (store_e != 0) the block's sum is taken relative to the row's shift
     // s_t, sum_v exp(z - s_t): one exp per logit serves both the sum and the stored E.  The
@@ -560,7 +562,7 @@ void lm_gemm_kernel(const GemmParams p) {
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       if (lane < 32) xmax[wm * kBN + cl] = mx;
       if (rel) {
-        float ssum = 0.0f;
+        float ssum = 0.0f, zsum = 0.0f;  // sum exp(z - s_t), sum exp(z - s_t) z
         T* e1 = static_cast<T*>(p.E1) + int64_t(t) * p.ldE1;
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi) {
@@ -573,6 +575,7 @@ void lm_gemm_kernel(const GemmParams p) {
               e[q] = __expf(acc[mi][ni][rg * 4 + q] - s_t);
               if (!rows_full && m0 + acc_row(wm, mi, rg * 4 + q, lane) >= Vr) e[q] = 0.0f;
               ssum += e[q];
+              zsum = fmaf(e[q], acc[mi][ni][rg * 4 + q], zsum);
             }
             if constexpr (sizeof(T) == 2) {
               typedef float f32x2_t __attribute__((ext_vector_type(2)));
@@ -601,7 +604,11 @@ void lm_gemm_kernel(const GemmParams p) {
           }
         }
         ssum += __shfl_xor(ssum, 32, 64);
-        if (lane < 32) xsum[wm * kBN + cl] = ssum;
+        zsum += __shfl_xor(zsum, 32, 64);
+        if (lane < 32) {
+          xsum[wm * kBN + cl] = ssum;
+          xsz[wm * kBN + cl] = zsum;
+        }
       }
     }
     __syncthreads();
@@ -610,16 +617,24 @@ void lm_gemm_kernel(const GemmParams p) {
       for (int ni = 0; ni < NI; ++ni) {
         const int cl = acc_col<T>(wn, ni, lane);
         const float M = fmaxf(xmax[cl], xmax[kBN + cl]);
-        float ssum = 0.0f;
+        float ssum = 0.0f, zsum = 0.0f;
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int v = m0 + acc_row(wm, mi, r, lane);
-            if (v < Vr) ssum += __expf(acc[mi][ni][r] - M);
+            if (v < Vr) {
+              const float ex = __expf(acc[mi][ni][r] - M);
+              ssum += ex;
+              zsum = fmaf(ex, acc[mi][ni][r], zsum);
+            }
           }
         ssum += __shfl_xor(ssum, 32, 64);
-        if (lane < 32) xsum[wm * kBN + cl] = ssum;
+        zsum += __shfl_xor(zsum, 32, 64);
+        if (lane < 32) {
+          xsum[wm * kBN + cl] = ssum;
+          xsz[wm * kBN + cl] = zsum;
+        }
       }
       __syncthreads();
     }
@@ -628,6 +643,7 @@ void lm_gemm_kernel(const GemmParams p) {
       if (t < p.N) {
         p.pmax[int64_t(mb) * p.ldp + t] = fmaxf(xmax[cl], xmax[kBN + cl]);
         p.psum[int64_t(mb) * p.ldp + t] = xsum[cl] + xsum[kBN + cl];
+        if (p.psz) p.psz[int64_t(mb) * p.ldp + t] = xsz[cl] + xsz[kBN + cl];
       }
     }
   } else if constexpr (MODE == MODE_DH) {
@@ -717,45 +733,60 @@ __global__ void slab_prep_kernel(const int32_t* __restrict__ token_ids,
 //             (exp(z - s_t) could leave float range) gets s_t = max and its token block is
 //             marked for a second evaluation.
 __global__ __launch_bounds__(256) void merge_kernel(
-    const float* __restrict__ pmax, const float* __restrict__ psum, int64_t ldp, int32_t nmb,
-    const float* __restrict__ zlab, const int32_t* __restrict__ yslab, int32_t Tc, int32_t rel,
-    int32_t check, float* __restrict__ lse_out, float* __restrict__ logp_out,
+    const float* __restrict__ pmax, const float* __restrict__ psum,
+    const float* __restrict__ psz, int64_t ldp, int32_t nmb, const float* __restrict__ zlab,
+    const int32_t* __restrict__ yslab, int32_t Tc, int32_t rel, int32_t check,
+    float* __restrict__ lse_out, float* __restrict__ logp_out, float* __restrict__ ent_out,
     float* __restrict__ shift, int32_t* __restrict__ redo_blk, int32_t* __restrict__ redo_count) {
-  __shared__ float sm[4][64], ss[4][64];
+  __shared__ float sm[4][64], ss[4][64], sz[4][64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int t = blockIdx.x * 64 + lane;
   const bool ok = t < Tc;
-  float M = -INFINITY, S = 0.0f;
+  const bool ent = psz != nullptr;
+  // S = sum exp(z - ref), Z = sum exp(z - ref) z, both relative to the same reference
+  float M = -INFINITY, S = 0.0f, Z = 0.0f;
   if (ok) {
     for (int b = wv; b < nmb; b += 4) {
       const float m = pmax[int64_t(b) * ldp + t];
       const float x = psum[int64_t(b) * ldp + t];
+      const float y = ent ? psz[int64_t(b) * ldp + t] : 0.0f;
       if (rel) {
         M = fmaxf(M, m);
         S += x;
+        Z += y;
       } else if (m > M) {
-        S = S * __expf(M - m) + x;
+        const float f = __expf(M - m);
+        S = S * f + x;
+        Z = Z * f + y;
         M = m;
       } else {
-        S += x * __expf(m - M);
+        const float f = __expf(m - M);
+        S += x * f;
+        Z += y * f;
       }
     }
   }
   sm[wv][lane] = M;
   ss[wv][lane] = S;
+  sz[wv][lane] = Z;
   __syncthreads();
   if (wv != 0 || !ok) return;
-  float Mt = sm[0][lane], St = ss[0][lane];
+  float Mt = sm[0][lane], St = ss[0][lane], Zt = sz[0][lane];
   for (int w = 1; w < 4; ++w) {
-    const float m = sm[w][lane], x = ss[w][lane];
+    const float m = sm[w][lane], x = ss[w][lane], y = sz[w][lane];
     if (rel) {
       Mt = fmaxf(Mt, m);
       St += x;
+      Zt += y;
     } else if (m > Mt) {
-      St = St * __expf(Mt - m) + x;
+      const float f = __expf(Mt - m);
+      St = St * f + x;
+      Zt = Zt * f + y;
       Mt = m;
     } else if (m > -INFINITY) {
-      St += x * __expf(m - Mt);
+      const float f = __expf(m - Mt);
+      St += x * f;
+      Zt += y * f;
     }
   }
   const float s_t = (rel && shift) ? shift[t] : 0.0f;
@@ -763,11 +794,30 @@ __global__ __launch_bounds__(256) void merge_kernel(
   const int y = yslab[t];
   if (lse_out) lse_out[t] = l;
   if (logp_out) logp_out[t] = y >= 0 ? zlab[t] - l : __int_as_float(0x7fc00000);
+  // entropy -sum_v p_v log p_v = lse - sum_v p_v z_v, sum_v p_v z_v = Z / S
+  if (ent_out) ent_out[t] = l - Zt / St;
   if (rel && check && !(Mt - s_t < 60.0f && Mt - s_t > -60.0f)) {
     shift[t] = Mt;
     redo_blk[t / kBN] = 1;
     atomicAdd(redo_count, 1);
   }
+}
+
+// sum of x[0..n) in float64, fixed order (one block): the mean entropy of the kept tokens
+__global__ __launch_bounds__(256) void sum_f32_kernel(const float* __restrict__ x, int64_t n,
+                                                      float* __restrict__ out) {
+  __shared__ double red[4];
+  double s = 0.0;
+  const int64_t per = (n + blockDim.x - 1) / blockDim.x;
+  const int64_t b = threadIdx.x * per, e = min(n, b + per);
+  for (int64_t i = b; i < e; ++i) s += double(x[i]);
+  // fixed-shape tree: wave butterfly, then the 4 wave sums in order
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0) red[wv] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) out[0] = float(((red[0] + red[1]) + red[2]) + red[3]);
 }
 
 __device__ __forceinline__ double block_sum_d(double v, double* red) {
@@ -1056,8 +1106,9 @@ static int token_logprob_impl(const void* hidden, const int32_t* row_index, cons
     FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, 2.0 * V * double(Tc) * d, stream)));
     const int32_t nmb = (V + kBM - 1) / kBM;
     hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 64)), dim3(256), 0, stream, w.pmax, w.psum,
-                       ch, nmb, w.zlab, w.yslab, Tc, 0, 0, lse ? lse + t0 : (float*)nullptr,
-                       logp + t0, (float*)nullptr, (int32_t*)nullptr, (int32_t*)nullptr);
+                       (const float*)nullptr, ch, nmb, w.zlab, w.yslab, Tc, 0, 0,
+                       lse ? lse + t0 : (float*)nullptr, logp + t0, (float*)nullptr,
+                       (float*)nullptr, (int32_t*)nullptr, (int32_t*)nullptr);
     FR_LAUNCHED();
   }
   return FASTRL_OK;
@@ -1115,7 +1166,7 @@ static SlabPlan plan_slabs(const int64_t* off, int32_t S, int64_t cap) {
 
 struct LossWs {
   void *WT, *E1, *Bd;
-  float *pmax, *psum, *zlab, *shift, *gslab, *cslab, *lse, *logp;
+  float *pmax, *psum, *psz, *ent, *zlab, *shift, *gslab, *cslab, *lse, *logp;
   int32_t *yslab, *redo_blk, *redo_count, *seq_clip, *lab_cnt, *lab_off, *lab_cur, *lab_tok;
   double* seq_loss;
 };
@@ -1131,6 +1182,10 @@ static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_
   w.Bd = dw ? c.take<char>(size_t(a.d) * tcp * esz) : nullptr;
   w.pmax = c.take<float>(size_t(nmb * tcp));
   w.psum = c.take<float>(size_t(nmb * tcp));
+  const bool ent = a.entropy != nullptr || a.entropy_sum != nullptr;
+  w.psz = ent ? c.take<float>(size_t(nmb * tcp)) : nullptr;
+  w.ent = a.entropy ? a.entropy
+                    : (a.entropy_sum ? c.take<float>(size_t(std::max<int64_t>(a.T, 1))) : nullptr);
   w.zlab = c.take<float>(size_t(tcp));
   w.shift = c.take<float>(size_t(tcp));
   w.gslab = c.take<float>(size_t(tcp));
@@ -1203,25 +1258,26 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
     p.A = a.W; p.lda = d; p.M = V;
     p.B = a.hidden; p.ldb = d; p.N = Tc; p.b_rows = a.row_index; p.b_row_base = t0;
     p.K = d;
-    p.pmax = w.pmax; p.psum = w.psum; p.ldp = tcp; p.zlab = w.zlab; p.yslab = w.yslab;
-    p.shift = w.shift; p.E1 = w.E1; p.ldE1 = Vpad;
+    p.pmax = w.pmax; p.psum = w.psum; p.psz = w.psz; p.ldp = tcp; p.zlab = w.zlab;
+    p.yslab = w.yslab; p.shift = w.shift; p.E1 = w.E1; p.ldE1 = Vpad;
     p.Vreal = V; p.store_e = (dh || dw) ? 1 : 0; p.status = a.status;
     p.redo_blk = w.redo_blk;
     const double f_fwd = 2.0 * double(V) * Tc * d;
     FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, f_fwd, stream)));
     const bool store = dh || dw;
     hipLaunchKernelGGL(merge_kernel, dim3(nb1d(std::max(Tc, 1), 64)), dim3(256), 0, stream,
-                       w.pmax, w.psum, tcp, nmb, w.zlab, w.yslab, Tc, store ? 1 : 0,
-                       store ? 1 : 0, w.lse + t0, w.logp + t0, store ? w.shift : (float*)nullptr,
-                       w.redo_blk, w.redo_count);
+                       w.pmax, w.psum, w.psz, tcp, nmb, w.zlab, w.yslab, Tc, store ? 1 : 0,
+                       store ? 1 : 0, w.lse + t0, w.logp + t0, w.ent ? w.ent + t0 : nullptr,
+                       store ? w.shift : (float*)nullptr, w.redo_blk, w.redo_count);
     FR_LAUNCHED();
     if (store) {
       // token blocks holding a row that needs a shift: evaluate again, then merge again
       p.store_e = 2;
       FR_TRY((launch_gemm<T, MODE_FWD>(p, -1, 0.0, stream)));
       hipLaunchKernelGGL(merge_kernel, dim3(nb1d(std::max(Tc, 1), 64)), dim3(256), 0, stream,
-                         w.pmax, w.psum, tcp, nmb, w.zlab, w.yslab, Tc, 1, 0, w.lse + t0,
-                         w.logp + t0, w.shift, w.redo_blk, w.redo_count);
+                         w.pmax, w.psum, w.psz, tcp, nmb, w.zlab, w.yslab, Tc, 1, 0, w.lse + t0,
+                         w.logp + t0, w.ent ? w.ent + t0 : nullptr, w.shift, w.redo_blk,
+                         w.redo_count);
       FR_LAUNCHED();
     }
     hipLaunchKernelGGL(loss_kernel, dim3(unsigned(s1 - s0)), dim3(256), 0, stream, w.logp,
@@ -1278,6 +1334,11 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
   hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, stream, w.seq_loss, w.seq_clip,
                      a.S, w.redo_count, a.loss, a.stats);
   FR_LAUNCHED();
+  if (a.entropy_sum) {
+    hipLaunchKernelGGL(sum_f32_kernel, dim3(1), dim3(256), 0, stream, w.ent, a.T,
+                       a.entropy_sum);
+    FR_LAUNCHED();
+  }
   return FASTRL_OK;
 }
 

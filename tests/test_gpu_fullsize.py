@@ -8,7 +8,7 @@ The oracle cannot evaluate every kept token at the 7B shape (up to 7.5e14 fp64 F
   sum_v dW[v] = 0 (relative to the one-hot part), <dW, W> = <dH, H>, and the reported loss
   equals the loss of the reported log-probs;
 * a slab of whole kept sequences (about 1K tokens) at full V x d runs through the same entry
-  point and is compared element by element, dW included.
+  point and is compared element by element, dW and the per-token entropy included.
 Old/ref log-probs are "current + N(0, 0.05)": exact oracle log-probs for every token the
 oracle checks, a plain-torch fp32 evaluation for the others.
 """
@@ -177,13 +177,16 @@ def test_full_config(fr, c):
                         ref_logp=t(ref2) if cfg.beta else None,
                         seq_index=t(ref["kept_traj"][:S2]), row_index=t(src[:T2].astype(np.int32)),
                         algo=cfg.algo, norm=cfg.norm, eps_low=cfg.eps_low, eps_high=cfg.eps_high,
-                        beta=cfg.beta, status=st).run()
+                        beta=cfg.beta, status=st, need_entropy=True).run()
     torch.cuda.synchronize()
     assert st.item() == 0
     lpg = call2.logp[:T2].double().cpu().numpy()
     assert np.abs(lpg - lp2).max() < LOGP_ATOL
     assert abs(call2.loss.item() - loss2) <= REL * max(abs(loss2), 1e-8)
     assert int(call2.stats[0].item()) == info2["clipped_tokens"]
+    ent2 = oracle.token_entropy(Hs2, W64)
+    assert np.abs(call2.entropy[:T2].double().cpu().numpy() - ent2).max() < 2e-3
+    assert abs(call2.entropy_sum.item() - ent2.sum()) <= 1e-4 * ent2.sum()
     dHg = call2.dhidden[:T2].double().cpu().numpy()
     dWg = call2.dW.double().cpu().numpy()
     dH1, dW1 = onehot_parts(Hs2, W64, y_all[:T2], g2)
