@@ -17,6 +17,7 @@ Differential-Aware Advantage Pruning with Adaptive Rollout Sampling for GRPO"):
 * ``loss``      -- GRPO / DAPO / GSPO clipped surrogate and its per-token gradient
                    coefficient (Sec. 3.1, Eq. 1, Eq. grad, clipping indicator)
 * ``ars``       -- adaptive rollout sampling controller (Sec. 3.3; Alg. 1 Phase 1)
+* ``optim``     -- the AdamW step on W consuming dW (Sec. 4.1 hyper-parameters)
 * ``pipeline``  -- one hot-path step end to end, in the order of Alg. 1
 
 Everything is float64 (rewards, hidden states and weights are read as the exact
@@ -30,6 +31,7 @@ from .mdap import (ngram_set, jaccard_counts, theta_below_tau, greedy_mdap_class
 from .lmhead import token_logprob, lmhead_backward, logits, token_entropy
 from .loss import policy_loss, token_weights
 from .ars import ARSController
+from .optim import adamw_step
 from .pipeline import hot_path_step
 
 __all__ = [
@@ -38,5 +40,5 @@ __all__ = [
     "continuous_classes", "visit_order",
     "token_logprob", "lmhead_backward", "logits", "token_entropy", "policy_loss",
     "token_weights",
-    "ARSController", "hot_path_step",
+    "ARSController", "hot_path_step", "adamw_step",
 ]
