@@ -11,6 +11,7 @@
  *                                                                 (Sec. 3.2, post-pruning evaluation)
  *   fastrl_policy_loss_fwd_bwd  GRPO/DAPO/GSPO clipped loss, backward to dhidden and dW
  *                                                                 (Sec. 3.1, Eq. 1, Eq. grad)
+ *   fastrl_adamw_step           AdamW update of W consuming dW    (Sec. 4.1; Alg. 1 update)
  *   fastrl_ars_*                adaptive rollout sampling, host only (Sec. 3.3; Alg. 1 Phase 1)
  *
  * Conventions shared by every entry point
@@ -69,6 +70,7 @@ typedef enum fastrl_status {
 #define FASTRL_SB_BAD_INDEX     0x20  /* row_index / seq_index entry out of range */
 #define FASTRL_SB_SHIFT_REDO    0x40  /* informational: some logits were re-evaluated with a
                                          per-token shift because exp(z) left float range */
+#define FASTRL_SB_BAD_GRAD      0x80  /* a non-finite gradient entry reached the optimizer */
 
 typedef enum fastrl_dtype { FASTRL_F32 = 0, FASTRL_BF16 = 1 } fastrl_dtype;
 typedef enum fastrl_algo { FASTRL_GRPO = 0, FASTRL_DAPO = 1, FASTRL_GSPO = 2 } fastrl_algo;
@@ -283,6 +285,26 @@ typedef struct fastrl_loss_args {
 size_t fastrl_loss_args_size(void);
 size_t fastrl_policy_loss_workspace_size(const fastrl_loss_args* args);
 int fastrl_policy_loss_fwd_bwd(const fastrl_loss_args* args, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * fastrl_adamw_step -- the policy update that consumes dW (Alg. 1, "update pi_theta"; the
+ * paper trains with AdamW, lr 1e-6, weight decay 1e-2, Sec. 4.1).  Decoupled weight decay
+ * with bias correction, per element, t = step (1-based), g = grad_scale * grad:
+ *   theta <- theta (1 - lr wd);  m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2
+ *   theta <- theta - (lr / (1 - beta1^t)) m / (sqrt(v) / sqrt(1 - beta2^t) + eps)
+ * float32 arithmetic on float32 master weights; theta, m, v are updated in place.
+ *   theta, m, v [n] float, device, 16-byte aligned (m = v = 0 before the first step);
+ *   grad [n] float, device, 16-byte aligned (e.g. dW from fastrl_policy_loss_fwd_bwd, after
+ *   any data-parallel reduction); w_bf16 [n] bfloat16 or NULL, 8-byte aligned: receives
+ *   round-to-nearest-even(theta) for the bf16 LM-head kernels.  n >= 0, step >= 1,
+ *   lr >= 0, 0 <= beta1, beta2 < 1, eps >= 0, weight_decay >= 0, all finite.
+ * A non-finite g sets FASTRL_SB_BAD_GRAD in status (the update still runs, as in the usual
+ * optimizers, and propagates the value).  No workspace.
+ * ------------------------------------------------------------------------------------ */
+int fastrl_adamw_step(float* theta, uint16_t* w_bf16, const float* grad, float* m, float* v,
+                      int64_t n, int64_t step, float lr, float beta1, float beta2, float eps,
+                      float weight_decay, float grad_scale, int32_t* status,
+                      hipStream_t stream);
 
 /* ------------------------------------------------------------------------------------
  * Adaptive Rollout Sampling (Sec. 3.3; Alg. 1 Phase 1(a)/(b)).  Host-only, plain data:

@@ -30,7 +30,7 @@ NORMS = {"seq_mean_token_mean": NORM_SEQ_MEAN_TOKEN_MEAN, "token_mean": NORM_TOK
 K_LOGITS_FWD, K_DHIDDEN, K_DW = 0, 1, 2
 STATUS_BITS = {0x1: "BAD_OFFSETS", 0x2: "BAD_TOKEN", 0x4: "GROUP_TOO_BIG",
                0x8: "SEQ_TOO_LONG", 0x10: "BAD_REWARD", 0x20: "BAD_INDEX",
-               0x40: "SHIFT_REDO"}
+               0x40: "SHIFT_REDO", 0x80: "BAD_GRAD"}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
@@ -89,6 +89,8 @@ _SIGS = {
     "fastrl_loss_args_size": (_sz, []),
     "fastrl_policy_loss_workspace_size": (_sz, [ctypes.POINTER(LossArgs)]),
     "fastrl_policy_loss_fwd_bwd": (ctypes.c_int, [ctypes.POINTER(LossArgs), _vp]),
+    "fastrl_adamw_step": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _f32, _f32,
+                                         _f32, _f32, _f32, _f32, _vp, _vp]),
     "fastrl_ars_init": (ctypes.c_int, [ctypes.POINTER(ARSState), _i32, _i64, _i64]),
     "fastrl_ars_next_n": (ctypes.c_int32, [ctypes.POINTER(ARSState)]),
     "fastrl_ars_observe": (ctypes.c_int, [ctypes.POINTER(ARSState), _vp, _vp, _i32]),
@@ -297,6 +299,21 @@ def policy_loss_fwd_bwd(*args, **kw):
     """One call of fastrl_policy_loss_fwd_bwd; returns the LossCall holding the outputs
     (loss, logp, lse, dhidden, dW, stats, and entropy / entropy_sum with need_entropy)."""
     return LossCall(*args, **kw).run()
+
+
+def adamw_step(theta, grad, m, v, *, step, lr=1e-6, betas=(0.9, 0.999), eps=1e-8,
+               weight_decay=1e-2, grad_scale=1.0, w_bf16=None, status=None):
+    """In-place AdamW update of float32 ``theta``, ``m``, ``v`` from ``grad`` (e.g. dW);
+    optionally writes the bfloat16 copy ``w_bf16``.  ``step`` is 1-based."""
+    n = theta.numel()
+    for t in (theta, grad, m, v):
+        assert t.dtype == torch.float32 and t.is_contiguous() and t.numel() == n
+    if w_bf16 is not None:
+        assert w_bf16.dtype == torch.bfloat16 and w_bf16.is_contiguous() and w_bf16.numel() == n
+    _check(_lib.fastrl_adamw_step(_p(theta), _p(w_bf16), _p(grad), _p(m), _p(v), n, int(step),
+                                  float(lr), float(betas[0]), float(betas[1]), float(eps),
+                                  float(weight_decay), float(grad_scale), _p(status),
+                                  _stream()), "fastrl_adamw_step")
 
 
 class ARS:

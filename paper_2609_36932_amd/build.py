@@ -8,7 +8,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfastrl.so")
-SOURCES = ["api.hip", "advantage.hip", "prune.hip", "lmhead.hip"]
+SOURCES = ["api.hip", "advantage.hip", "prune.hip", "lmhead.hip", "optim.hip"]
 ARCH = os.environ.get("FASTRL_ARCH", "gfx950")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
          "-Wno-unused-function", "-Wno-unused-variable",

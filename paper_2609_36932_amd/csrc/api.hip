@@ -22,6 +22,9 @@ size_t token_logprob_workspace(int64_t T, int32_t d, int32_t V, int32_t dtype);
 int run_token_logprob(const void*, const int32_t*, const void*, int32_t, int64_t, int32_t,
                       int32_t, const int32_t*, float*, float*, int32_t*, void*, hipStream_t);
 size_t policy_loss_workspace(const fastrl_loss_args& a);
+int launch_adamw(float* theta, uint16_t* wbf, const float* grad, float* mom, float* var,
+                 int64_t n, int64_t step, float lr, float beta1, float beta2, float eps,
+                 float weight_decay, float grad_scale, int32_t* status, hipStream_t stream);
 int run_policy_loss(const fastrl_loss_args& a, hipStream_t stream);
 
 static thread_local std::string g_err;
@@ -70,7 +73,7 @@ using namespace fastrl;
 extern "C" {
 
 const char* fastrl_last_error(void) { return g_err.c_str(); }
-int fastrl_version(void) { return 10000; }
+int fastrl_version(void) { return 10100; }
 
 int fastrl_advantage(const float* rewards, const int32_t* group_off, int32_t Q, int32_t N,
                      int32_t std_ddof, float eps, int32_t drop_uniform, float* adv,
@@ -347,6 +350,31 @@ int fastrl_profile_read(int32_t kind, double* total_ms, int64_t* launches, doubl
   *launches = n;
   *flops = fl;
   return FASTRL_OK;
+}
+
+int fastrl_adamw_step(float* theta, uint16_t* w_bf16, const float* grad, float* m, float* v,
+                      int64_t n, int64_t step, float lr, float beta1, float beta2, float eps,
+                      float weight_decay, float grad_scale, int32_t* status,
+                      hipStream_t stream) {
+  clear_error();
+  FR_CHECK_ARG(n >= 0 && step >= 1, FASTRL_ERR_SHAPE, "fastrl_adamw_step: need n >= 0, step >= 1");
+  FR_CHECK_ARG(std::isfinite(lr) && lr >= 0 && std::isfinite(eps) && eps >= 0 &&
+                   std::isfinite(weight_decay) && weight_decay >= 0 &&
+                   std::isfinite(grad_scale) && beta1 >= 0 && beta1 < 1 && beta2 >= 0 &&
+                   beta2 < 1,
+               FASTRL_ERR_VALUE,
+               "fastrl_adamw_step: need finite lr, eps, weight_decay, grad_scale >= 0 (except "
+               "grad_scale) and betas in [0, 1)");
+  if (n == 0) return FASTRL_OK;
+  FR_CHECK_ARG(theta && grad && m && v, FASTRL_ERR_NULL_PTR,
+               "fastrl_adamw_step: theta / grad / m / v is NULL");
+  auto al = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; };
+  FR_CHECK_ARG(al(theta, 16) && al(grad, 16) && al(m, 16) && al(v, 16) &&
+                   (w_bf16 == nullptr || al(w_bf16, 8)),
+               FASTRL_ERR_VALUE,
+               "fastrl_adamw_step: theta / grad / m / v must be 16-byte aligned, w_bf16 8-byte");
+  return launch_adamw(theta, w_bf16, grad, m, v, n, step, lr, beta1, beta2, eps, weight_decay,
+                      grad_scale, status, stream);
 }
 
 }  // extern "C"

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(fr):
 def test_struct_layout(fr):
     assert fr._lib.fastrl_loss_args_size() == ctypes.sizeof(fr.LossArgs)
     assert fr._lib.fastrl_prune_args_size() == ctypes.sizeof(fr.PruneArgs)
-    assert fr._lib.fastrl_version() >= 10000
+    assert fr._lib.fastrl_version() >= 10100
 
 
 def test_host_validation_errors(fr):
@@ -82,6 +82,16 @@ def test_host_validation_errors(fr):
     pa.group_eps = 0.0
     assert L.fastrl_prune_ex(ctypes.byref(pa), None) == -1       # class_id needed
     assert b"class_id" in L.fastrl_last_error()
+    # fastrl_adamw_step
+    ok = (1e-6, 0.9, 0.999, 1e-8, 1e-2, 1.0)
+    assert L.fastrl_adamw_step(None, None, None, None, None, 0, 1, *ok, None, None) == 0
+    assert L.fastrl_adamw_step(None, None, None, None, None, 10, 0, *ok, None, None) == -2
+    assert L.fastrl_adamw_step(None, None, None, None, None, 10, 1, *ok, None, None) == -1
+    assert L.fastrl_adamw_step(None, None, None, None, None, 10, 1, 1e-6, 1.0, 0.999, 1e-8,
+                               1e-2, 1.0, None, None) == -3
+    p = ctypes.c_void_p(256)
+    q = ctypes.c_void_p(260)   # not 16-byte aligned
+    assert L.fastrl_adamw_step(p, None, q, p, p, 10, 1, *ok, None, None) == -3
     # dtype / shape checks of the LM-head entry points
     assert L.fastrl_token_logprob(None, None, None, 7, 1, 16, 10, None, None, None, None,
                                   None, 0, None) == -4
