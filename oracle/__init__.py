@@ -27,7 +27,7 @@ float64 values of their stored float32 / bfloat16 bits).  Integer decisions
 from .advantage import group_advantage
 from .mdap import (ngram_set, jaccard_counts, theta_below_tau, greedy_mdap_class,
                    budget_keep, prune_prompt, prune_batch, compact, continuous_classes,
-                   visit_order)
+                   visit_order, dp_align_fill)
 from .lmhead import token_logprob, lmhead_backward, logits, token_entropy
 from .loss import policy_loss, token_weights
 from .ars import ARSController
@@ -37,7 +37,7 @@ from .pipeline import hot_path_step
 __all__ = [
     "group_advantage", "ngram_set", "jaccard_counts", "theta_below_tau",
     "greedy_mdap_class", "budget_keep", "prune_prompt", "prune_batch", "compact",
-    "continuous_classes", "visit_order",
+    "continuous_classes", "visit_order", "dp_align_fill",
     "token_logprob", "lmhead_backward", "logits", "token_entropy", "policy_loss",
     "token_weights",
     "ARSController", "hot_path_step", "adamw_step",

@@ -27,6 +27,10 @@ Readings where the paper is silent or ambiguous:
 * questions marked invalid (DAPO drop of all-equal groups) keep nothing and report
   an MDAP count of 0.
 
+DP alignment (Alg. 1, after the union of the per-question sets): while the kept count
+is not a multiple of the data-parallel divisor d, add the unselected trajectory with the
+highest |A|, round-robin over the questions (``dp_align_fill``).
+
 Continuous rewards (appendix on the grounding task; the only change the paper makes
 for continuous rewards is to Eq. grouping): o_i and o_j share an advantage group
 whenever |A_i - A_j| < eps (eps = 1e-4 there).  Readings:
@@ -214,6 +218,41 @@ def prune_batch(token_ids, traj_tok_off, rewards, group_off, class_id, group_val
     if return_classes:
         return keep, counts, used
     return keep, counts
+
+
+def dp_align_fill(keep_mask, adv, group_off, group_valid, d):
+    """Alg. 1 DP alignment: while |S| mod d != 0, add an unselected trajectory with the
+    highest |A|, round-robin over the questions.  Readings: one round visits the valid
+    questions in index order and adds each one's best remaining unselected trajectory
+    (|A| descending, float32 values, ties by lowest index); rounds repeat until |S| is a
+    multiple of d or no unselected trajectory is left.  Returns (keep uint8[N], added)."""
+    keep = np.array(keep_mask, dtype=np.uint8)
+    d = int(d)
+    if d <= 1:
+        return keep, 0
+    a = np.abs(np.asarray(adv, dtype=np.float32).astype(np.float64))
+    off = np.asarray(group_off, dtype=np.int64)
+    Q = len(off) - 1
+    pools = []
+    for q in range(Q):
+        if group_valid is not None and not group_valid[q]:
+            pools.append([])
+            continue
+        cand = [i for i in range(int(off[q]), int(off[q + 1])) if not keep[i]]
+        pools.append(sorted(cand, key=lambda i: (-a[i], i)))
+    added = 0
+    while int(keep.sum()) % d != 0:
+        progressed = False
+        for q in range(Q):
+            if int(keep.sum()) % d == 0:
+                break
+            if pools[q]:
+                keep[pools[q].pop(0)] = 1
+                added += 1
+                progressed = True
+        if not progressed:
+            break
+    return keep, added
 
 
 def compact(keep_mask, traj_tok_off):

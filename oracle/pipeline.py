@@ -9,7 +9,7 @@ infrastructure only; see oracle/__init__):
 import numpy as np
 
 from .advantage import group_advantage
-from .mdap import prune_batch, compact
+from .mdap import prune_batch, compact, dp_align_fill
 from .lmhead import token_logprob, lmhead_backward
 from .loss import policy_loss
 
@@ -18,9 +18,11 @@ def hot_path_step(rewards, group_off, token_ids, traj_tok_off, *, H=None, W=None
                   old_logp=None, ref_logp=None, algo="grpo",
                   norm="seq_mean_token_mean", eps_low=0.2, eps_high=0.2, beta=0.0,
                   ngram_n=1, tau_num=4, tau_den=5, keep_ratio=0.0,
-                  drop_uniform=False, std_ddof=1, adv_eps=1e-6, group_eps=0.0, lmhead=True):
+                  drop_uniform=False, std_ddof=1, adv_eps=1e-6, group_eps=0.0, dp_align=1,
+                  lmhead=True):
     """``group_eps`` > 0: continuous-reward groups |A_i - A_j| < group_eps (appendix on
-    the grounding task) instead of bit-equal reward classes."""
+    the grounding task) instead of bit-equal reward classes.  ``dp_align`` > 1: Alg. 1's
+    fill of the kept set up to a multiple of the data-parallel divisor."""
     out = {}
     adv, cls, valid = group_advantage(rewards, group_off, ddof=std_ddof, eps=adv_eps,
                                       drop_uniform=drop_uniform)
@@ -31,7 +33,8 @@ def hot_path_step(rewards, group_off, token_ids, traj_tok_off, *, H=None, W=None
                                      ngram_n=ngram_n, tau_num=tau_num, tau_den=tau_den,
                                      keep_ratio=keep_ratio, adv=adv32, group_eps=group_eps,
                                      return_classes=True)
-    out.update(keep_mask=keep, mdap_count=counts, prune_class=used)
+    keep, added = dp_align_fill(keep, adv32, group_off, valid, dp_align)
+    out.update(keep_mask=keep, mdap_count=counts, prune_class=used, dp_added=added)
     kept, koff, src = compact(keep, traj_tok_off)
     out.update(kept_traj=kept, kept_tok_off=koff, tok_src=src)
     if not lmhead:
