@@ -71,6 +71,8 @@ typedef enum fastrl_status {
 #define FASTRL_SB_SHIFT_REDO    0x40  /* informational: some logits were re-evaluated with a
                                          per-token shift because exp(z) left float range */
 #define FASTRL_SB_BAD_GRAD      0x80  /* a non-finite gradient entry reached the optimizer */
+#define FASTRL_SB_FILL_SHORT    0x100 /* DP alignment: too few unselected trajectories to reach
+                                         a multiple of dp_align */
 
 typedef enum fastrl_dtype { FASTRL_F32 = 0, FASTRL_BF16 = 1 } fastrl_dtype;
 typedef enum fastrl_algo { FASTRL_GRPO = 0, FASTRL_DAPO = 1, FASTRL_GSPO = 2 } fastrl_algo;
@@ -163,6 +165,13 @@ int fastrl_prune(const int32_t* token_ids, const int64_t* traj_tok_off, int64_t 
  *              lowest member index.  class_id is then ignored and may be NULL; adv is required.
  *              Non-finite adv values are treated as 0 and set FASTRL_SB_BAD_REWARD.
  *   class_out  [N] int32, device, or NULL: the class id each trajectory was pruned under.
+ *   dp_align   0 or 1: off.  d > 1 (<= 4096): Alg. 1's alignment to d data-parallel ranks,
+ *              after MDAP and the budget: while the kept count is not a multiple of d, the
+ *              unselected trajectory with the highest |A| is added, round-robin over the
+ *              valid questions in index order (one per question per round, |A| descending,
+ *              ties by index).  Needs adv.  If too few unselected trajectories are left, all
+ *              of them are added and FASTRL_SB_FILL_SHORT is set.  mdap_count is the MDAP
+ *              count before the fill (what ARS observes).
  * fastrl_prune_args_size() returns sizeof(fastrl_prune_args) for binding checks.
  * Errors as fastrl_prune; group_eps must be finite and >= 0 (FASTRL_ERR_VALUE).
  * ------------------------------------------------------------------------------------ */
@@ -188,6 +197,7 @@ typedef struct fastrl_prune_args {
   const float* adv;
   double group_eps;
   int32_t* class_out;
+  int32_t dp_align;
 } fastrl_prune_args;
 size_t fastrl_prune_args_size(void);
 int fastrl_prune_ex(const fastrl_prune_args* args, hipStream_t stream);

@@ -30,7 +30,7 @@ NORMS = {"seq_mean_token_mean": NORM_SEQ_MEAN_TOKEN_MEAN, "token_mean": NORM_TOK
 K_LOGITS_FWD, K_DHIDDEN, K_DW = 0, 1, 2
 STATUS_BITS = {0x1: "BAD_OFFSETS", 0x2: "BAD_TOKEN", 0x4: "GROUP_TOO_BIG",
                0x8: "SEQ_TOO_LONG", 0x10: "BAD_REWARD", 0x20: "BAD_INDEX",
-               0x40: "SHIFT_REDO", 0x80: "BAD_GRAD"}
+               0x40: "SHIFT_REDO", 0x80: "BAD_GRAD", 0x100: "FILL_SHORT"}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
@@ -62,7 +62,7 @@ class PruneArgs(ctypes.Structure):
         ("tau_num", _i32), ("tau_den", _i32), ("keep_ratio", _f64), ("keep_mask", _vp),
         ("mdap_count", _vp), ("kept_traj", _vp), ("kept_tok_off", _vp), ("tok_src", _vp),
         ("counts", _vp), ("status", _vp), ("ws", _vp), ("ws_bytes", _sz), ("adv", _vp),
-        ("group_eps", _f64), ("class_out", _vp),
+        ("group_eps", _f64), ("class_out", _vp), ("dp_align", _i32),
     ]
 
 
@@ -165,13 +165,15 @@ def advantage(rewards, group_off, std_ddof=1, eps=1e-6, drop_uniform=False, stat
 
 def prune(token_ids, traj_tok_off, rewards, group_off, class_id, group_valid, *, V,
           max_group, max_len, ngram_n=1, tau=(4, 5), keep_ratio=0.0, adv=None, group_eps=0.0,
-          class_out=False, status=None):
+          class_out=False, dp_align=0, status=None):
     """MDAP + budget + compaction.  Returns a dict of device tensors (see fastrl.h).
 
     ``adv`` (the advantages) sets Alg. 1's traversal order (|A| descending); with
     ``group_eps`` > 0 the classes are the continuous-reward groups |A_i - A_j| < group_eps
     and ``class_id`` is ignored; ``class_out`` adds the class ids used to the result.  The
-    plain call (no adv, no group_eps, no class_out) goes through ``fastrl_prune``."""
+    plain call (no adv, no group_eps, no class_out) goes through ``fastrl_prune``.
+    ``dp_align`` > 1 fills the kept set up to a multiple of that many data-parallel ranks
+    (Alg. 1; needs ``adv``)."""
     dev = rewards.device
     Q = group_off.numel() - 1
     N = rewards.numel()
@@ -186,7 +188,7 @@ def prune(token_ids, traj_tok_off, rewards, group_off, class_id, group_valid, *,
     )
     ws_n = _lib.fastrl_prune_workspace_size(Q, N, T_total, max_group, ngram_n)
     ws = _workspace(ws_n, dev)
-    if adv is None and not group_eps and not class_out:
+    if adv is None and not group_eps and not class_out and dp_align <= 1:
         _check(_lib.fastrl_prune(
             _p(token_ids), _p(traj_tok_off), T_total, _p(rewards), _p(group_off), _p(class_id),
             _p(group_valid), Q, N, max_group, max_len, V, ngram_n, int(tau[0]), int(tau[1]),
@@ -208,6 +210,7 @@ def prune(token_ids, traj_tok_off, rewards, group_off, class_id, group_valid, *,
     a.ws, a.ws_bytes = _p(ws), ws.numel()
     a.adv, a.group_eps = _p(adv), float(group_eps)
     a.class_out = _p(out["class_id"]) if class_out else None
+    a.dp_align = int(dp_align)
     _check(_lib.fastrl_prune_ex(ctypes.byref(a), _stream()), "fastrl_prune_ex")
     return out
 
@@ -363,7 +366,7 @@ def hot_path_step(rewards, group_off, token_ids, traj_tok_off, hidden, W, old_lo
                   norm="seq_mean_token_mean", eps_low=0.2, eps_high=0.2, beta=0.0,
                   ngram_n=1, tau=(4, 5), keep_ratio=0.0, drop_uniform=False,
                   need_dhidden=True, need_dW=True, slab_tokens=0, status=None,
-                  dhidden_dtype=None, group_eps=0.0):
+                  dhidden_dtype=None, group_eps=0.0, dp_align=0):
     """advantage -> prune + compaction -> (one device->host read of the kept counts and
     offsets) -> loss forward/backward on the kept tokens.  Returns a dict.  ``group_eps``
     > 0 prunes under continuous-reward groups |A_i - A_j| < group_eps."""
@@ -371,7 +374,8 @@ def hot_path_step(rewards, group_off, token_ids, traj_tok_off, hidden, W, old_lo
     pr = prune(token_ids, traj_tok_off, rewards, group_off, cls, valid, V=V,
                max_group=max_group, max_len=max_len, ngram_n=ngram_n, tau=tau,
                keep_ratio=keep_ratio, status=status,
-               adv=adv if group_eps else None, group_eps=group_eps)
+               adv=adv if (group_eps or dp_align > 1) else None, group_eps=group_eps,
+               dp_align=dp_align)
     counts = pr["counts"].cpu()
     n_kept, t_kept = int(counts[0]), int(counts[1])
     koff_host = pr["kept_tok_off"][:n_kept + 1].cpu()

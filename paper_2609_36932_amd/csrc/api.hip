@@ -16,8 +16,8 @@ size_t prune_workspace(int32_t Q, int32_t N, int64_t T_total, int32_t max_group)
 int launch_prune(const int32_t*, const int64_t*, int64_t, const float*, const int32_t*,
                  const int32_t*, const float*, double, const uint8_t*, int32_t, int32_t,
                  int32_t, int32_t, int32_t, int32_t, int32_t, int32_t, double, uint8_t*,
-                 int32_t*, int32_t*, int32_t*, int64_t*, int32_t*, int64_t*, int32_t*, void*,
-                 hipStream_t);
+                 int32_t*, int32_t*, int32_t, int32_t*, int64_t*, int32_t*, int64_t*, int32_t*,
+                 void*, hipStream_t);
 size_t token_logprob_workspace(int64_t T, int32_t d, int32_t V, int32_t dtype);
 int run_token_logprob(const void*, const int32_t*, const void*, int32_t, int64_t, int32_t,
                       int32_t, const int32_t*, float*, float*, int32_t*, void*, hipStream_t);
@@ -129,6 +129,10 @@ static int check_and_prune(const fastrl_prune_args& a, hipStream_t stream) {
                std::string(fn) + ": class_id is NULL (needed unless group_eps > 0)");
   FR_CHECK_ARG(a.N == 0 || !(a.group_eps > 0.0) || a.adv, FASTRL_ERR_NULL_PTR,
                std::string(fn) + ": group_eps > 0 needs adv");
+  FR_CHECK_ARG(a.dp_align >= 0 && a.dp_align <= 4096, FASTRL_ERR_VALUE,
+               std::string(fn) + ": dp_align must be in [0, 4096]");
+  FR_CHECK_ARG(a.N == 0 || a.dp_align <= 1 || a.adv, FASTRL_ERR_NULL_PTR,
+               std::string(fn) + ": dp_align > 1 needs adv");
   FR_CHECK_ARG(a.Q == 0 || (a.group_off && a.mdap_count), FASTRL_ERR_NULL_PTR,
                std::string(fn) + ": group_off / mdap_count is NULL");
   FR_CHECK_ARG(a.T_total == 0 || (a.token_ids && a.tok_src), FASTRL_ERR_NULL_PTR,
@@ -140,7 +144,8 @@ static int check_and_prune(const fastrl_prune_args& a, hipStream_t stream) {
   return launch_prune(a.token_ids, a.traj_tok_off, a.T_total, a.rewards, a.group_off,
                       a.class_id, a.adv, a.group_eps, a.group_valid, a.Q, a.N, a.max_group,
                       a.max_len, a.V, a.ngram_n, a.tau_num, a.tau_den, a.keep_ratio,
-                      a.keep_mask, a.mdap_count, a.class_out, a.kept_traj, a.kept_tok_off,
+                      a.keep_mask, a.mdap_count, a.class_out, a.dp_align, a.kept_traj,
+                      a.kept_tok_off,
                       a.tok_src, a.counts, a.status, a.ws, stream);
 }
 

@@ -12,6 +12,7 @@
 //                   order (|A| descending, ties by index, when advantages are given; else
 //                   ascending index), then the budget as "keep the K smallest (tier, rank,
 //                   class position) keys" -- the same list a class round-robin produces.
+//   K3b dp_fill     (optional) Alg. 1's DP alignment of the kept count, one block.
 //   K4 compaction   exclusive scans of kept flags and kept lengths (one block), then a
 //                   coalesced fill of tok_src, one block per kept trajectory.
 #include "common.h"
@@ -364,6 +365,81 @@ __global__ __launch_bounds__(64) void select_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------- K3b
+// DP alignment (Alg. 1 after the union of the per-question sets): while the kept count is
+// not a multiple of d, add the unselected trajectory with the highest |A|, round-robin over
+// the questions.  One block: count the kept set; rank every unselected member of a valid
+// question by (|A| descending, index); one thread deals the rounds to get t_q, the number of
+// members question q contributes; members of rank < t_q are kept.
+__global__ __launch_bounds__(1024) void dp_fill_kernel(
+    uint8_t* __restrict__ keep_mask, const float* __restrict__ adv,
+    const int32_t* __restrict__ group_off, const uint8_t* __restrict__ group_valid, int32_t Q,
+    int32_t N, int32_t max_group, int32_t d, int32_t* __restrict__ frank,
+    int32_t* __restrict__ unsel, int32_t* __restrict__ take, int32_t* __restrict__ status) {
+  __shared__ int32_t red[16];
+  __shared__ int32_t need_s;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int c = 0;
+  for (int i = tid; i < N; i += blockDim.x) c += keep_mask[i] ? 1 : 0;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o, 64);
+  if (lane == 0) red[wv] = c;
+  __syncthreads();
+  if (tid == 0) {
+    int kept = 0;
+    for (int w = 0; w < int(blockDim.x >> 6); ++w) kept += red[w];
+    need_s = (d - kept % d) % d;
+  }
+  __syncthreads();
+  if (need_s == 0) return;
+  for (int q = tid; q < Q; q += blockDim.x) {
+    const int g0 = group_off[q], g1 = group_off[q + 1];
+    int u = 0;
+    const bool ok = g0 >= 0 && g1 >= g0 && g1 <= N && g1 - g0 <= max_group &&
+                    (group_valid == nullptr || group_valid[q] != 0);
+    if (ok) {
+      for (int i = g0; i < g1; ++i) {
+        if (keep_mask[i]) continue;
+        const float ai = isfinite(adv[i]) ? fabsf(adv[i]) : 0.0f;
+        int r = 0;
+        for (int j = g0; j < g1; ++j) {
+          if (keep_mask[j]) continue;
+          const float aj = isfinite(adv[j]) ? fabsf(adv[j]) : 0.0f;
+          r += (aj > ai) || (aj == ai && j < i);
+        }
+        frank[i] = r;
+        ++u;
+      }
+    }
+    unsel[q] = u;
+    take[q] = 0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int need = need_s;
+    for (int r = 0; need > 0; ++r) {
+      bool any = false;
+      for (int q = 0; q < Q && need > 0; ++q) {
+        if (unsel[q] > r) {
+          take[q] = r + 1;
+          --need;
+          any = true;
+        }
+      }
+      if (!any) break;
+    }
+    if (need > 0) set_status(status, FASTRL_SB_FILL_SHORT);
+  }
+  __syncthreads();
+  for (int q = tid; q < Q; q += blockDim.x) {
+    const int t = take[q];
+    if (t == 0) continue;
+    const int g0 = group_off[q], g1 = group_off[q + 1];
+    for (int i = g0; i < g1; ++i)
+      if (!keep_mask[i] && frank[i] < t) keep_mask[i] = 1;  // ranks were taken above
+  }
+}
+
 // ---------------------------------------------------------------------------- K4
 __global__ __launch_bounds__(1024) void compact_scan_kernel(
     const uint8_t* __restrict__ keep_mask, const int64_t* __restrict__ toff, int32_t N,
@@ -448,6 +524,9 @@ size_t prune_workspace(int32_t Q, int32_t N, int64_t T_total, int32_t max_group)
   c.take<uint8_t>(size_t(Q > 0 ? Q : 1) * max_group * max_group);
   c.take<int32_t>(size_t(N + 1));
   c.take<int32_t>(size_t(N + 1));
+  c.take<int32_t>(size_t(N + 1));
+  c.take<int32_t>(size_t(Q + 1));
+  c.take<int32_t>(size_t(Q + 1));
   return c.size();
 }
 
@@ -456,7 +535,7 @@ int launch_prune(const int32_t* token_ids, const int64_t* toff, int64_t T_total,
                  const float* adv, double group_eps, const uint8_t* group_valid, int32_t Q,
                  int32_t N, int32_t max_group, int32_t max_len, int32_t V, int32_t ngram_n,
                  int32_t tau_num, int32_t tau_den, double keep_ratio, uint8_t* keep_mask,
-                 int32_t* mdap_count, int32_t* class_out, int32_t* kept_traj,
+                 int32_t* mdap_count, int32_t* class_out, int32_t dp_align, int32_t* kept_traj,
                  int64_t* kept_tok_off, int32_t* tok_src, int64_t* counts, int32_t* status,
                  void* ws, hipStream_t stream) {
   Carver c(ws);
@@ -465,6 +544,9 @@ int launch_prune(const int32_t* token_ids, const int64_t* toff, int64_t T_total,
   uint8_t* conflict = c.take<uint8_t>(size_t(Q > 0 ? Q : 1) * max_group * max_group);
   int32_t* kpos = c.take<int32_t>(size_t(N + 1));
   int32_t* cls_eps = c.take<int32_t>(size_t(N + 1));
+  int32_t* frank = c.take<int32_t>(size_t(N + 1));
+  int32_t* unsel = c.take<int32_t>(size_t(Q + 1));
+  int32_t* take = c.take<int32_t>(size_t(Q + 1));
   const int32_t* cls = class_id;
   if (group_eps > 0.0 && Q > 0) {
     hipLaunchKernelGGL(group_eps_kernel, dim3(Q), dim3(64), 0, stream, adv, group_off, N,
@@ -490,6 +572,12 @@ int launch_prune(const int32_t* token_ids, const int64_t* toff, int64_t T_total,
                        adv, group_valid, N, max_group, keep_ratio, conflict, keep_mask,
                        mdap_count, class_out, status);
     FR_LAUNCHED();
+    if (dp_align > 1) {
+      hipLaunchKernelGGL(dp_fill_kernel, dim3(1), dim3(1024), 0, stream, keep_mask, adv,
+                         group_off, group_valid, Q, N, max_group, dp_align, frank, unsel, take,
+                         status);
+      FR_LAUNCHED();
+    }
   }
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(1024), 0, stream, keep_mask, toff, N,
                      kept_traj, kept_tok_off, kpos, counts);

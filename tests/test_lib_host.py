@@ -82,6 +82,12 @@ def test_host_validation_errors(fr):
     pa.group_eps = 0.0
     assert L.fastrl_prune_ex(ctypes.byref(pa), None) == -1       # class_id needed
     assert b"class_id" in L.fastrl_last_error()
+    pa.class_id = dummy
+    pa.dp_align = -2
+    assert L.fastrl_prune_ex(ctypes.byref(pa), None) == -3
+    pa.dp_align = 8
+    assert L.fastrl_prune_ex(ctypes.byref(pa), None) == -1       # dp_align > 1 without adv
+    assert b"dp_align" in L.fastrl_last_error()
     # fastrl_adamw_step
     ok = (1e-6, 0.9, 0.999, 1e-8, 1e-2, 1.0)
     assert L.fastrl_adamw_step(None, None, None, None, None, 0, 1, *ok, None, None) == 0
