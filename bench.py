@@ -12,9 +12,13 @@ clip 0.2, keep ratio 0.5):
 Inputs are resident in HBM before timing.  The reported value is kept tokens per second
 of the whole step.  ``roofline`` describes the dominant kernel, timed with HIP events on
 its launch stream during the timed steps; ``cpu_baseline`` times the fp64 oracle on a
-bounded sample of the same workload.
+bounded sample of the same workload.  ``rows`` (after the timed steps, skipped with
+--no-rows) times the parts beyond the step on the same workload: pruning with
+continuous-reward groups, the DP-alignment fill, the entropy accumulator (one loss call with
+and without it) and the AdamW update of W (bytes per second against HBM).
 
 usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 3] [--no-cpu]
+                       [--no-rows]
 """
 import argparse
 import json
@@ -40,6 +44,8 @@ def parse():
     ap.add_argument("--slab", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=768)
+    ap.add_argument("--no-rows", action="store_true",
+                    help="skip the timings of the additional rows")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one plain device-to-device copy of this many MiB (a "
                          "known-size reference for the HBM byte counters)")
@@ -141,6 +147,95 @@ def cpu_baseline(cfg, ro, inp, n_tokens):
                        f"{S} kept sequences ({len(src)} tokens); {dt:.1f} s")
 
 
+def _time_gpu(fn, reps):
+    """Average ms of fn() over reps calls on the current stream (HIP events)."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    b.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def extra_rows(cfg, ro, inp, fr, max_group, max_len, last, args):
+    """Timings of the rows beyond the hot path, on the same workload: pruning with
+    continuous-reward groups, the entropy accumulator, the AdamW step on W, the DP fill."""
+    import torch
+    import oracle
+    from synth import continuous_rewards
+    dev = inp["H"].device
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+    rows = {}
+    # N1: continuous groups |A_i - A_j| < 1e-4 (continuous rewards of the same batch shape)
+    rw = continuous_rewards(ro.group_off, seed=cfg.seed)
+    rw_d = t(rw)
+    adv, cls, valid = fr.advantage(rw_d, inp["group_off"])
+    kw = dict(V=cfg.V, max_group=max_group, max_len=max_len, keep_ratio=cfg.keep_ratio)
+    plain = _time_gpu(lambda: fr.prune(inp["token_ids"], inp["traj_tok_off"], rw_d,
+                                       inp["group_off"], cls, valid, **kw), 20)
+    cont = _time_gpu(lambda: fr.prune(inp["token_ids"], inp["traj_tok_off"], rw_d,
+                                      inp["group_off"], cls, valid, adv=adv, group_eps=1e-4,
+                                      **kw), 20)
+    t0 = time.perf_counter()
+    oracle.hot_path_step(rw, ro.group_off, ro.token_ids, ro.traj_tok_off, lmhead=False,
+                         keep_ratio=cfg.keep_ratio, group_eps=1e-4)
+    rows["continuous_groups_prune"] = dict(
+        ms=cont, ms_bit_equal_classes=plain, oracle_s=time.perf_counter() - t0,
+        note="fastrl_prune_ex, eps 1e-4, whole batch incl. compaction; latency-bound")
+    # N4: DP fill to a multiple of 8 ranks
+    fill = _time_gpu(lambda: fr.prune(inp["token_ids"], inp["traj_tok_off"], rw_d,
+                                      inp["group_off"], cls, valid, adv=adv, dp_align=8,
+                                      **kw), 20)
+    rows["dp_align_fill_prune"] = dict(ms=fill, ms_without=plain, d=8)
+    # N2: entropy fused into the log-sum-exp pass: one loss call of the timed step with and
+    # without the extra accumulator
+    call = last["call"]
+    koff = last["kept_tok_off_host"]
+    pr = last["prune"]
+    mk = lambda ent: fr.LossCall(inp["H"], inp["W"], inp["token_ids"], inp["old"],
+                                 pr["kept_tok_off"], koff, last["adv"], ref_logp=inp["ref"],
+                                 seq_index=pr["kept_traj"], row_index=pr["tok_src"],
+                                 algo=cfg.algo, norm=cfg.norm, eps_low=cfg.eps_low,
+                                 eps_high=cfg.eps_high, beta=cfg.beta, T=last["t_kept"],
+                                 need_entropy=ent, slab_tokens=args.slab)
+    del call
+    c0 = mk(False)
+    base_ms = _time_gpu(c0.run, 1)
+    del c0
+    torch.cuda.empty_cache()
+    c1 = mk(True)
+    ent_ms = _time_gpu(c1.run, 1)
+    mean_ent = float(c1.entropy_sum.item()) / max(last["t_kept"], 1)
+    del c1
+    torch.cuda.empty_cache()
+    rows["entropy_in_lse_pass"] = dict(ms_loss_call=ent_ms, ms_loss_call_without=base_ms,
+                                       overhead=ent_ms / base_ms - 1.0,
+                                       mean_entropy=mean_ent)
+    # N3: AdamW on W (float32 master, moments, dW; bf16 copy): 30 bytes per parameter
+    n = cfg.V * cfg.d
+    th = inp["W"].float().reshape(-1).contiguous()
+    g = torch.empty_like(th).normal_(0, 1e-3)
+    m, v = torch.zeros_like(th), torch.zeros_like(th)
+    wb = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    ms = _time_gpu(lambda: fr.adamw_step(th, g, m, v, step=1, w_bf16=wb), 10)
+    gbs = 30.0 * n / (ms * 1e-3) / 1e9
+    sample = 1 << 22
+    th_h, g_h = th[:sample].double().cpu().numpy(), g[:sample].double().cpu().numpy()
+    t0 = time.perf_counter()
+    oracle.adamw_step(th_h, g_h, np.zeros(sample), np.zeros(sample), 1)
+    o_s = time.perf_counter() - t0
+    rows["adamw_W"] = dict(ms=ms, params=n, bytes_per_param=30, achieved_GBps=gbs,
+                           hbm_peak_GBps=8000.0, frac=gbs / 8000.0,
+                           oracle_params_per_s=sample / o_s)
+    del th, g, m, v, wb
+    torch.cuda.empty_cache()
+    return rows
+
+
 def torch_index(src, dev):
     import torch
     return torch.from_numpy(np.ascontiguousarray(src)).long().to(dev)
@@ -234,6 +329,9 @@ def main():
         "kernels": per,
         "gemm_ms_per_step": gemm_ms,
     }
+    if not args.no_rows:
+        log("[bench] timing the additional rows (continuous groups, entropy, AdamW, DP fill)")
+        res["rows"] = extra_rows(cfg, ro, inp, fr, max_group, max_len, out, args)
     if not args.no_cpu:
         log("[bench] timing the oracle on a CPU sample")
         res["cpu_baseline"] = cpu_baseline(cfg, ro, inp, args.cpu_tokens)

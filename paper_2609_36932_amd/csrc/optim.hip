@@ -32,35 +32,63 @@ __device__ __forceinline__ void adamw_one(float& th, float& m, float& v, float g
   th = __fsub_rn(th, __fmul_rn(c.step_size, __fdiv_rn(m, den)));
 }
 
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// Two 16-byte vectors of each stream per thread and iteration (all loads issued before the
+// arithmetic), non-temporal loads and stores (the 16+ GB stream would only evict the caches):
+// measured at the rate of a plain device copy on this part.
 __global__ __launch_bounds__(256) void adamw_kernel(float* __restrict__ theta,
                                                     uint16_t* __restrict__ wbf,
                                                     const float* __restrict__ grad,
                                                     float* __restrict__ mom,
                                                     float* __restrict__ var, int64_t n,
                                                     AdamWConst c, int32_t* __restrict__ status) {
+  constexpr int U = 2;
   const int64_t n4 = n >> 2;
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  f32x4_t* T = reinterpret_cast<f32x4_t*>(theta);
+  const f32x4_t* G = reinterpret_cast<const f32x4_t*>(grad);
+  f32x4_t* M = reinterpret_cast<f32x4_t*>(mom);
+  f32x4_t* V = reinterpret_cast<f32x4_t*>(var);
+  u32x2_t* WB = reinterpret_cast<u32x2_t*>(wbf);
   int bad = 0;
-  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n4; i += stride) {
-    float4 th = reinterpret_cast<const float4*>(theta)[i];
-    const float4 gr = reinterpret_cast<const float4*>(grad)[i];
-    float4 m = reinterpret_cast<const float4*>(mom)[i];
-    float4 v = reinterpret_cast<const float4*>(var)[i];
-    const float g0 = gr.x * c.gscale, g1 = gr.y * c.gscale, g2 = gr.z * c.gscale,
-                g3 = gr.w * c.gscale;
-    bad |= !(isfinite(g0) && isfinite(g1) && isfinite(g2) && isfinite(g3));
-    adamw_one(th.x, m.x, v.x, g0, c);
-    adamw_one(th.y, m.y, v.y, g1, c);
-    adamw_one(th.z, m.z, v.z, g2, c);
-    adamw_one(th.w, m.w, v.w, g3, c);
-    reinterpret_cast<float4*>(theta)[i] = th;
-    reinterpret_cast<float4*>(mom)[i] = m;
-    reinterpret_cast<float4*>(var)[i] = v;
-    if (wbf) {
-      uint2 pk;
-      pk.x = uint32_t(f32_to_bf16(th.x)) | (uint32_t(f32_to_bf16(th.y)) << 16);
-      pk.y = uint32_t(f32_to_bf16(th.z)) | (uint32_t(f32_to_bf16(th.w)) << 16);
-      reinterpret_cast<uint2*>(wbf)[i] = pk;
+  for (int64_t i0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i0 < n4; i0 += stride * U) {
+    f32x4_t th[U], g[U], m[U], v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = i0 + u * stride;
+      if (i < n4) {
+        th[u] = __builtin_nontemporal_load(T + i);
+        g[u] = __builtin_nontemporal_load(G + i);
+        m[u] = __builtin_nontemporal_load(M + i);
+        v[u] = __builtin_nontemporal_load(V + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = i0 + u * stride;
+      if (i < n4) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float a = th[u][q], mm = m[u][q], vv = v[u][q];
+          const float gg = g[u][q] * c.gscale;
+          bad |= !isfinite(gg);
+          adamw_one(a, mm, vv, gg, c);
+          th[u][q] = a;
+          m[u][q] = mm;
+          v[u][q] = vv;
+        }
+        __builtin_nontemporal_store(th[u], T + i);
+        __builtin_nontemporal_store(m[u], M + i);
+        __builtin_nontemporal_store(v[u], V + i);
+        if (wbf) {
+          u32x2_t pk;
+          pk[0] = uint32_t(f32_to_bf16(th[u][0])) | (uint32_t(f32_to_bf16(th[u][1])) << 16);
+          pk[1] = uint32_t(f32_to_bf16(th[u][2])) | (uint32_t(f32_to_bf16(th[u][3])) << 16);
+          __builtin_nontemporal_store(pk, WB + i);
+        }
+      }
     }
   }
   // the last n % 4 elements
@@ -95,7 +123,7 @@ int launch_adamw(float* theta, uint16_t* wbf, const float* grad, float* mom, flo
   c.eps = eps;
   c.gscale = grad_scale;
   const int64_t n4 = std::max<int64_t>(n >> 2, 1);
-  const unsigned blocks = unsigned(std::min<int64_t>((n4 + 255) / 256, 256 * 8));
+  const unsigned blocks = unsigned(std::min<int64_t>((n4 + 255) / 256, 65536));
   hipLaunchKernelGGL(adamw_kernel, dim3(blocks), dim3(256), 0, stream, theta, wbf, grad, mom,
                      var, n, c, status);
   FR_LAUNCHED();
