@@ -254,13 +254,13 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   const int tg = lane >> 4, ti = lane & 15;
   const int tr_k = 8 * (tg >> 1) + (ti >> 2);
   const int tr_m = 16 * (tg & 1) + 4 * (ti & 3);
-  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2]) {
+  // A fragments i0 .. i1-1 of k-step kk
+  auto frags_a = [&](int stage, int kk, bf16x8_t (&fa)[4], int i0, int i1) {
     const uint16_t* as = smem + stage * 2 * TILE;
-    const uint16_t* bs = as + TILE;
     const int slot = ((kk * 2 + (lane >> 5)) ^ sw) * 8;
     if (A_KMAJOR) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = i0; i < i1; ++i) {
         const int m = wm * 128 + i * 32 + tr_m;
         s16x4_t h[2];
 #pragma unroll
@@ -281,12 +281,20 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = i0; i < i1; ++i)
         fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 32 + (lane & 31)) * BK + slot);
     }
+  };
+  auto frags_b = [&](int stage, int kk, bf16x8_t (&fb)[2]) {
+    const uint16_t* bs = smem + stage * 2 * TILE + TILE;
+    const int slot = ((kk * 2 + (lane >> 5)) ^ sw) * 8;
 #pragma unroll
     for (int j = 0; j < 2; ++j)
       fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 64 + j * 32 + (lane & 31)) * BK + slot);
+  };
+  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2]) {
+    frags_a(stage, kk, fa, 0, 4);
+    frags_b(stage, kk, fb);
   };
   auto mma = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[2]) {
 #pragma unroll
@@ -314,6 +322,12 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
                      "+v"(fb[1])::"memory");
   };
 
+  auto mma_row = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[2], int i) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
+
   bf16x8_t fa0[4], fb0[2], fa1[4], fb1[2];
   // pin the order inside a k-step: the 8 MFMAs of this step with the fragment reads of
   // the next step spread among them (at most one step's reads in flight, so the wait before
@@ -325,6 +339,31 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);         \
   __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                 \
   __builtin_amdgcn_sched_barrier(0)
+  // one full k-step: the MFMAs of step kk (fragments fa, fb) with the reads of step kk + 1
+  // (into na, nb) spread among them.  The transposing reads of K-major A are inline asm, which
+  // the scheduling groups do not place: they are pinned between the MFMAs of rows 0, 1, 2-3.
+  auto kstep = [&](int stage, int kk_next, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2],
+                   bf16x8_t (&na)[4], bf16x8_t (&nb)[2]) {
+    wait_a(fa, fb);
+    if (A_KMAJOR) {
+      frags_b(stage, kk_next, nb);
+      mma_row(fa, fb, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      frags_a(stage, kk_next, na, 0, 2);
+      __builtin_amdgcn_sched_barrier(0);
+      mma_row(fa, fb, 1);
+      __builtin_amdgcn_sched_barrier(0);
+      frags_a(stage, kk_next, na, 2, 4);
+      __builtin_amdgcn_sched_barrier(0);
+      mma_row(fa, fb, 2);
+      mma_row(fa, fb, 3);
+      __builtin_amdgcn_sched_barrier(0);
+    } else {
+      frags(stage, kk_next, na, nb);
+      mma(fa, fb);
+      FR_STEP_ORDER();
+    }
+  };
   issue(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   if (nk == 1 && ktail) zero_tail(0, 0);
@@ -334,18 +373,9 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   int kt = 0;
   for (; kt + 1 < nk; ++kt) {
     const int cur = kt & 1;
-    wait_a(fa0, fb0);
-    frags(cur, 1, fa1, fb1);
-    mma(fa0, fb0);
-    FR_STEP_ORDER();
-    wait_a(fa1, fb1);
-    frags(cur, 2, fa0, fb0);
-    mma(fa1, fb1);
-    FR_STEP_ORDER();
-    wait_a(fa0, fb0);
-    frags(cur, 3, fa1, fb1);
-    mma(fa0, fb0);
-    FR_STEP_ORDER();
+    kstep(cur, 1, fa0, fb0, fa1, fb1);
+    kstep(cur, 2, fa1, fb1, fa0, fb0);
+    kstep(cur, 3, fa0, fb0, fa1, fb1);
     // last k-step: half of its MFMAs cover the barrier; the other half cover the next
     // tile's load issue and the first fragment reads of tile kt+1
     wait_a(fa1, fb1);
@@ -372,18 +402,9 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the re-load above has landed
   {  // last tile
     const int cur = kt & 1;
-    wait_a(fa0, fb0);
-    frags(cur, 1, fa1, fb1);
-    mma(fa0, fb0);
-    FR_STEP_ORDER();
-    wait_a(fa1, fb1);
-    frags(cur, 2, fa0, fb0);
-    mma(fa1, fb1);
-    FR_STEP_ORDER();
-    wait_a(fa0, fb0);
-    frags(cur, 3, fa1, fb1);
-    mma(fa0, fb0);
-    FR_STEP_ORDER();
+    kstep(cur, 1, fa0, fb0, fa1, fb1);
+    kstep(cur, 2, fa1, fb1, fa0, fb0);
+    kstep(cur, 3, fa0, fb0, fa1, fb1);
     wait_a(fa1, fb1);
     mma(fa1, fb1);
   }
