@@ -247,3 +247,28 @@ def test_empty_and_single_token(fr):
     assert abs(call.loss.item() - loss) < 1e-2 * abs(loss)
     assert rel_fro(call.dW.double().cpu().numpy(), dW) < REL
     assert rel_fro(call.dhidden[:1].double().cpu().numpy(), dH) < REL
+
+
+@pytest.mark.parametrize("which", ["dhidden_only", "dW_only"])
+def test_single_backward_gemm(fr, which):
+    """One backward GEMM alone (its own launch) gives the same gradient as the joint launch."""
+    pb = Problem(3, DEV, Q=4, len_range=(20, 90), V=1000, d=136)
+    ref = pb.oracle_loss()
+    pr = pb.pr
+    cfg = pb.cfg
+    call = fr.LossCall(
+        pb.H_poisoned.to(DEV), pb.W.to(DEV), to_dev(pb.ro.token_ids, DEV), to_dev(pb.old, DEV),
+        to_dev(pr["kept_tok_off"], DEV), torch.from_numpy(pr["kept_tok_off"]),
+        to_dev(pr["adv"].astype(np.float32), DEV), ref_logp=to_dev(pb.ref, DEV),
+        seq_index=to_dev(pr["kept_traj"].astype(np.int32), DEV),
+        row_index=to_dev(pb.src.astype(np.int32), DEV), algo=cfg.algo, norm=cfg.norm,
+        eps_low=cfg.eps_low, eps_high=cfg.eps_high, beta=cfg.beta,
+        need_dhidden=which == "dhidden_only", need_dW=which == "dW_only").run()
+    torch.cuda.synchronize()
+    T = len(pb.src)
+    if which == "dhidden_only":
+        assert call.dW is None
+        assert rel_fro(call.dhidden[:T].double().cpu().numpy(), ref["dH"]) < REL
+    else:
+        assert call.dhidden is None
+        assert rel_fro(call.dW.double().cpu().numpy(), ref["dW"]) < REL
