@@ -123,6 +123,20 @@ def _p(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _arg(t, dtype, name):
+    """Pointer of a caller tensor after checking that the library can read it as the dense
+    device array fastrl.h describes (None passes through as NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise FastRLError(f"{name}: expected a device tensor")
+    if not t.is_contiguous():
+        raise FastRLError(f"{name}: expected a contiguous tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise FastRLError(f"{name}: expected {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
 def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -157,9 +171,11 @@ def advantage(rewards, group_off, std_ddof=1, eps=1e-6, drop_uniform=False, stat
     adv = torch.empty(N, dtype=torch.float32, device=rewards.device)
     cls = torch.empty(N, dtype=torch.int32, device=rewards.device)
     valid = torch.empty(Q, dtype=torch.uint8, device=rewards.device)
-    _check(_lib.fastrl_advantage(_p(rewards), _p(group_off), Q, N, std_ddof, eps,
+    _check(_lib.fastrl_advantage(_arg(rewards, torch.float32, "rewards"),
+                                 _arg(group_off, torch.int32, "group_off"), Q, N, std_ddof, eps,
                                  int(bool(drop_uniform)), _p(adv), _p(cls), _p(valid),
-                                 _p(status), _stream()), "fastrl_advantage")
+                                 _arg(status, torch.int32, "status"), _stream()),
+           "fastrl_advantage")
     return adv, cls, valid
 
 
@@ -178,6 +194,12 @@ def prune(token_ids, traj_tok_off, rewards, group_off, class_id, group_valid, *,
     Q = group_off.numel() - 1
     N = rewards.numel()
     T_total = token_ids.numel()
+    for t, dt, nm in ((token_ids, torch.int32, "token_ids"), (traj_tok_off, torch.int64,
+                      "traj_tok_off"), (rewards, torch.float32, "rewards"),
+                      (group_off, torch.int32, "group_off"), (class_id, torch.int32, "class_id"),
+                      (group_valid, torch.uint8, "group_valid"), (adv, torch.float32, "adv"),
+                      (status, torch.int32, "status")):
+        _arg(t, dt, nm)
     out = dict(
         keep_mask=torch.empty(N, dtype=torch.uint8, device=dev),
         mdap_count=torch.empty(max(Q, 0), dtype=torch.int32, device=dev),
@@ -221,6 +243,12 @@ def token_logprob(hidden, W, token_ids, row_index=None, T=None, status=None):
     dt = _dtype_code(hidden)
     d = hidden.shape[1]
     V = W.shape[0]
+    for t, dty, nm in ((hidden, hidden.dtype, "hidden"), (W, hidden.dtype, "W"),
+                       (token_ids, torch.int32, "token_ids"), (row_index, torch.int32,
+                       "row_index"), (status, torch.int32, "status")):
+        _arg(t, dty, nm)
+    if W.shape[1] != d:
+        raise FastRLError("W must be [V, d] with the hidden size of `hidden`")
     if T is None:
         T = row_index.numel() if row_index is not None else hidden.shape[0]
     logp = torch.empty(max(T, 1), dtype=torch.float32, device=hidden.device)
@@ -246,6 +274,16 @@ class LossCall:
         dt = _dtype_code(hidden)
         d = hidden.shape[1]
         V = W.shape[0]
+        for t, dty, nm in ((hidden, hidden.dtype, "hidden"), (W, hidden.dtype, "W"),
+                           (token_ids, torch.int32, "token_ids"),
+                           (old_logp, torch.float32, "old_logp"),
+                           (ref_logp, torch.float32, "ref_logp"), (seq_off, torch.int64, "seq_off"),
+                           (adv, torch.float32, "adv"), (seq_index, torch.int32, "seq_index"),
+                           (row_index, torch.int32, "row_index"), (dW, torch.float32, "dW"),
+                           (status, torch.int32, "status")):
+            _arg(t, dty, nm)
+        if W.shape[1] != d:
+            raise FastRLError("W must be [V, d] with the hidden size of `hidden`")
         self.seq_off_host = seq_off_host.to(torch.int64).contiguous().cpu()
         S = self.seq_off_host.numel() - 1
         T = int(self.seq_off_host[-1]) if T is None else T
@@ -309,10 +347,14 @@ def adamw_step(theta, grad, m, v, *, step, lr=1e-6, betas=(0.9, 0.999), eps=1e-8
     """In-place AdamW update of float32 ``theta``, ``m``, ``v`` from ``grad`` (e.g. dW);
     optionally writes the bfloat16 copy ``w_bf16``.  ``step`` is 1-based."""
     n = theta.numel()
-    for t in (theta, grad, m, v):
-        assert t.dtype == torch.float32 and t.is_contiguous() and t.numel() == n
-    if w_bf16 is not None:
-        assert w_bf16.dtype == torch.bfloat16 and w_bf16.is_contiguous() and w_bf16.numel() == n
+    for t, nm in ((theta, "theta"), (grad, "grad"), (m, "m"), (v, "v")):
+        _arg(t, torch.float32, nm)
+        if t.numel() != n:
+            raise FastRLError(f"{nm}: expected {n} elements")
+    _arg(w_bf16, torch.bfloat16, "w_bf16")
+    _arg(status, torch.int32, "status")
+    if w_bf16 is not None and w_bf16.numel() != n:
+        raise FastRLError(f"w_bf16: expected {n} elements")
     _check(_lib.fastrl_adamw_step(_p(theta), _p(w_bf16), _p(grad), _p(m), _p(v), n, int(step),
                                   float(lr), float(betas[0]), float(betas[1]), float(eps),
                                   float(weight_decay), float(grad_scale), _p(status),

@@ -182,3 +182,14 @@ def test_ars_bad_args(fr):
     st = fr.ARSState()
     assert fr._lib.fastrl_ars_init(ctypes.byref(st), 1, 10, 2) == -3
     assert fr._lib.fastrl_ars_init(None, 8, 10, 2) == -1
+
+
+def test_binding_rejects_host_tensors(fr):
+    """Every tensor handed to the library must be a dense device array: host tensors are
+    refused before any call reaches the library."""
+    import torch
+    assert fr._arg(None, torch.int32, "x") is None
+    with pytest.raises(fr.FastRLError, match="device tensor"):
+        fr._arg(torch.zeros(4, dtype=torch.int32), torch.int32, "x")
+    with pytest.raises(fr.FastRLError, match="device tensor"):
+        fr.advantage(torch.zeros(4), torch.tensor([0, 4], dtype=torch.int32))
