@@ -38,16 +38,15 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 256, kBN = 256;
 
-// wavefront geometry of the 256 x 256 block tile
-template <typename T>
-struct Geo;
-template <>
-struct Geo<uint16_t> {  // bf16: 8 wavefronts (two per SIMD) of 128 x 64
-  static constexpr int THREADS = 512, WAVES_N = 4, NI = 2, WPE = 2;
-};
-template <>
-struct Geo<float> {     // f32: 4 wavefronts of 128 x 128
-  static constexpr int THREADS = 256, WAVES_N = 2, NI = 4, WPE = 1;
+enum GemmMode { MODE_FWD = 0, MODE_DH = 1, MODE_DW = 2 };
+
+// wavefront geometry of the 256 x 256 block tile: the bf16 logits GEMM runs 8 wavefronts
+// (two per SIMD) of 128 x 64, every other GEMM 4 wavefronts of 128 x 128
+template <typename T, int MODE>
+struct Geo {
+  static constexpr bool W8 = sizeof(T) == 2 && MODE == MODE_FWD;
+  static constexpr int THREADS = W8 ? 512 : 256, WAVES_N = W8 ? 4 : 2, NI = W8 ? 2 : 4,
+                       WPE = W8 ? 2 : 1;
 };
 
 template <typename T>
@@ -69,8 +68,6 @@ struct Eng<float> {        // float32 operands
   static constexpr int VEC = 4;
   static constexpr int KSTEP = 2;
 };
-
-enum GemmMode { MODE_FWD = 0, MODE_DH = 1, MODE_DW = 2 };
 
 struct GemmParams {
   const void* A;            // [M, lda]
@@ -155,35 +152,238 @@ __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 __device__ __forceinline__ int acc_row(int wm, int mi, int r, int lane) {
   return wm * 128 + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
 }
-template <typename T>
+template <typename T, int MODE>
 __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
-  return wn * (kBN / Geo<T>::WAVES_N) + ni * 32 + (lane & 31);
+  return wn * (kBN / Geo<T, MODE>::WAVES_N) + ni * 32 + (lane & 31);
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
-// bf16 main loop.  Eight wavefronts (two per SIMD, so one can issue MFMAs while the
-// other waits on memory) each own a 128 x 64 part of the block tile.  LDS holds two stages
-// of a 256 x 64 A tile and a 256 x 64 B tile (32 KB each), written by direct global->LDS
-// loads (global_load_lds_dwordx4): one load instruction moves 1 KB, lane l writing its
-// 16-byte slot l; each wavefront moves 4 KB of each operand per tile.  Tile kt+1 is in flight
-// while tile kt is multiplied; fragments of k-step kk+1 are read while the MFMAs of k-step kk
-// run.
+// bf16 main loop of the backward GEMMs.  Four wavefronts (one per SIMD) each own a 128 x 128 part of the block tile.
+// Operand tiles of 64 k move global -> registers -> LDS through two register sets and two LDS
+// stages (a 256 x 64 A tile and a 256 x 64 B tile, 64 KB per stage).  Iteration kt:
+//   k-steps 0-1  MFMAs of tile kt; loads of tile kt+2 into register set kt % 2
+//   k-step 2     MFMAs of tile kt; tile kt+1 (register set (kt+1) % 2, loaded during iteration
+//                kt-1) written to LDS stage (kt+1) % 2, which nobody reads since the last barrier
+//   k-step 3     half of the MFMAs, barrier, the first fragments of tile kt+1 read under the
+//                other half
+// A load thus has more than one iteration to land, and every wait on memory is the compiler's
+// own vmcnt / lgkmcnt wait for the registers an instruction reads.  Inside each k-step the 16
+// MFMAs are interleaved with the next k-step's 8 fragment reads and the step's loads or LDS
+// writes.
 //
 // K-contiguous operand (rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
-// c ^ ((r >> 1) & 7).  The LDS serves a 16-byte-per-lane read 16 lanes (256 B, 64 banks) at a
-// time, and rows r..r+15 of a fragment then land on 16 distinct 16-byte bank groups.
+// c ^ ((r >> 1) & 7).  A fragment read (16 lanes = 16 rows of one chunk per LDS cycle) lands on
+// 16 distinct 16-byte bank groups, and a staging write covers whole rows (8 lanes per row).
 //
 // K-major A (A_KMAJOR: A[m][k] stored at k * lda + m, i.e. the logits-exp tile E[t][v] read
 // as E^T for dW): the tile is 64 rows of k x 256 m (512 B), row k keeping its m-chunk c in
 // slot c ^ ((k & 3) << 2).  Fragments come from ds_read_b64_tr_b16: inside each 16-lane group,
 // source lane j reads 4 consecutive m of row kbase + j/4 at m = mbase + 4 (j % 4), and lane i
 // receives A[mbase + i][kbase .. kbase + 3] -- 4 consecutive k of one row m, as the MFMA wants.
+constexpr int kTileP = kBM * 64;  // elements per operand per stage
+
+// K is a multiple of 64 (the backward GEMMs run over the padded vocabulary or slab), and the
+// leading dimensions stay below 8M elements (checked at launch).
 template <int MODE, bool A_KMAJOR>
 __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n0,
-                                              f32x16_t (&acc)[4][2], uint16_t* smem) {
+                                              f32x16_t (&acc)[4][4], uint16_t* smem) {
+  static_assert(MODE != MODE_FWD, "the logits GEMM runs the 8-wavefront engine");
+  constexpr int BK = 64;
+  constexpr int TILE = kTileP;
+  constexpr int STAGE = 2 * TILE;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int K = p.K;
+  const int nk = (K + BK - 1) / BK;
+
+  // staging: load j (0..7) of a K-contiguous operand moves row 32 j + tid / 8, k-chunk tid % 8;
+  // of the K-major A, k row 8 j + tid / 32, m-chunk tid % 32.  Row addresses are 32-bit element
+  // offsets from a per-block base (a block spans 256 rows), except the gathered rows of the
+  // logits' B operand, which keep full pointers.
+  const int srow = tid >> 3, sch = tid & 7;
+  const int krow = tid >> 5, mch = tid & 31;
+  const char* Ab = reinterpret_cast<const char*>(static_cast<const uint16_t*>(p.A) +
+                                                 (A_KMAJOR ? int64_t(m0) : int64_t(m0) * p.lda));
+  const char* Bb = reinterpret_cast<const char*>(static_cast<const uint16_t*>(p.B) +
+                                                 int64_t(n0) * p.ldb);
+  // byte offsets of this lane's 16-byte chunks from the tile base (below 2^32 for any
+  // leading dimension under 8M elements)
+  uint32_t ao[8], bo[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int r = 32 * j + srow;
+    // rows past the edge load a valid row; their results are never stored
+    ao[j] = A_KMAJOR ? (uint32_t(krow + 8 * j) * uint32_t(p.lda) + mch * 8) * 2
+                     : (uint32_t(min(r, p.M - 1 - m0)) * uint32_t(p.lda) + sch * 8) * 2;
+    bo[j] = (uint32_t(min(r, p.N - 1 - n0)) * uint32_t(p.ldb) + sch * 8) * 2;
+  }
+  const int64_t a_tile = A_KMAJOR ? int64_t(BK) * p.lda * 2 : BK * 2;  // bytes per k-tile
+
+  // loads j = 4 h .. 4 h + 3 of tile kt
+  auto load_half = [&](int kt, int h, u32x4_t (&ra)[8], u32x4_t (&rb)[8]) {
+    const char* At = Ab + kt * a_tile;
+    const char* Bt = Bb + kt * (BK * 2);
+#pragma unroll
+    for (int j = 4 * h; j < 4 * h + 4; ++j) {
+      ra[j] = *reinterpret_cast<const u32x4_t*>(At + ao[j]);
+      rb[j] = *reinterpret_cast<const u32x4_t*>(Bt + bo[j]);
+    }
+  };
+  // LDS slots this lane writes (operand-relative; load j adds 32 j rows, or 8 j k-rows)
+  const int wk = srow * BK + (sch ^ ((srow >> 1) & 7)) * 8;
+  constexpr int WJ = 32 * BK;  // elements between staging rows j, j+1
+  const int wkm = krow * kBM + (mch ^ ((krow & 3) << 2)) * 8;
+  auto write_tile = [&](int stage, const u32x4_t (&ra)[8], const u32x4_t (&rb)[8]) {
+    uint16_t* sa = smem + stage * STAGE;
+    uint16_t* sb = sa + TILE;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      *reinterpret_cast<u32x4_t*>(sa + (A_KMAJOR ? wkm + j * 8 * kBM : wk + j * WJ)) = ra[j];
+      *reinterpret_cast<u32x4_t*>(sb + wk + j * WJ) = rb[j];
+    }
+  };
+
+  // K-major A fragment source: group g = lane / 16, i = lane % 16 reads row
+  // k = 8 (g / 2) + 4 s + i / 4 (s = first / second half of the 8 k), m = 16 (g % 2) + 4 (i % 4)
+  const int tg = lane >> 4, ti = lane & 15;
+  const int tr_k = 8 * (tg >> 1) + (ti >> 2);
+  const int tr_m = 16 * (tg & 1) + 4 * (ti & 3);
+  // issued in the order the MFMAs consume them: A row 0, the B columns, A rows 1-3
+  auto read_frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[4]) {
+    const uint16_t* as = smem + stage * STAGE;
+    const uint16_t* bs = as + TILE;
+    // row (lane & 31) of a 32-row block, half lane / 32, of sub-tile kk
+    const int fo = (lane & 31) * BK + ((kk * 2 + (lane >> 5)) ^ ((lane >> 1) & 7)) * 8;
+    constexpr int RS = BK;  // row stride
+    auto read_a = [&](int i) {
+      if (A_KMAJOR) {
+        const int m = wm * 128 + i * 32 + tr_m;
+        s16x4_t h[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int k = kk * 16 + tr_k + 4 * hh;
+          const int c = (m >> 3) ^ ((k & 3) << 2);
+          h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_s16x4_t*)(as + k * kBM + c * 8 + (m & 7)));
+        }
+        typedef short s16x8_t __attribute__((ext_vector_type(8)));
+        const s16x8_t v = {h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
+        fa[i] = __builtin_bit_cast(bf16x8_t, v);
+      } else {
+        fa[i] = *reinterpret_cast<const bf16x8_t*>(as + fo + (wm * 128 + i * 32) * RS);
+      }
+    };
+    read_a(0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + fo + (wn * 128 + j * 32) * RS);
+#pragma unroll
+    for (int i = 1; i < 4; ++i) read_a(i);
+  };
+  auto mma_rows = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4], int i0, int i1) {
+#pragma unroll
+    for (int i = i0; i < i1; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
+  // fragment reads of one k-step (8, or 12 with the transposing A reads)
+  constexpr int NFR = A_KMAJOR ? 12 : 8;
+  constexpr int NFR_SLOT = (NFR + 7) / 8;  // reads per interleave slot (8 slots per k-step)
+
+  // one k-step's order: the next k-step's fragment reads and `n` instructions of class `mask`
+  // (global loads or LDS writes) alternate between the 16 MFMAs
+#define ORDER_READS_THEN(mask, n)                                     \
+  do {                                                                \
+    _Pragma("unroll") for (int q_ = 0; q_ < 8; ++q_) {                \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              \
+      __builtin_amdgcn_sched_group_barrier(0x100, NFR_SLOT, 0);       \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              \
+      __builtin_amdgcn_sched_group_barrier(mask, n, 0);               \
+    }                                                                 \
+  } while (0)
+  bf16x8_t fa0[4], fb0[4], fa1[4], fb1[4];
+  u32x4_t ra0[8], rb0[8], ra1[8], rb1[8];
+  auto iteration = [&](auto stage, int kt, u32x4_t (&la)[8], u32x4_t (&lb)[8], u32x4_t (&wa)[8],
+                       u32x4_t (&wb)[8]) {
+    constexpr int cur = decltype(stage)::value;
+    // the last iterations re-load and re-write the last tile into the unused stage (never
+    // read): keeps every iteration branch-free so its loads interleave with the MFMAs
+    const int tl = min(kt + 2, nk - 1);
+    // ---- k-step 0: loads of tile kt+2, first half
+    read_frags(cur, 1, fa1, fb1);
+    load_half(tl, 0, la, lb);
+    mma_rows(fa0, fb0, 0, 4);
+    ORDER_READS_THEN(0x020, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- k-step 1: second half
+    read_frags(cur, 2, fa0, fb0);
+    load_half(tl, 1, la, lb);
+    mma_rows(fa1, fb1, 0, 4);
+    ORDER_READS_THEN(0x020, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- k-step 2: tile kt+1 to the other stage
+    read_frags(cur, 3, fa1, fb1);
+    write_tile(cur ^ 1, wa, wb);
+    mma_rows(fa0, fb0, 0, 4);
+    ORDER_READS_THEN(0x200, 2);
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- k-step 3: half the MFMAs cover the write completion and the barrier, the other
+    // half the first fragment reads of tile kt+1
+    mma_rows(fa1, fb1, 0, 2);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    read_frags(cur ^ 1, 0, fa0, fb0);
+    mma_rows(fa1, fb1, 2, 4);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, NFR_SLOT, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // prologue: tile 0 in stage 0, tile 1 in flight in register set 1
+  load_half(0, 0, ra0, rb0);
+  load_half(0, 1, ra0, rb0);
+  load_half(min(1, nk - 1), 0, ra1, rb1);
+  load_half(min(1, nk - 1), 1, ra1, rb1);
+  write_tile(0, ra0, rb0);
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  read_frags(0, 0, fa0, fb0);
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    iteration(std::integral_constant<int, 0>{}, kt, ra0, rb0, ra1, rb1);
+    iteration(std::integral_constant<int, 1>{}, kt + 1, ra1, rb1, ra0, rb0);
+  }
+  if (kt < nk) iteration(std::integral_constant<int, 0>{}, kt, ra0, rb0, ra1, rb1);
+#undef ORDER_READS_THEN
+}
+
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// bf16 main loop of the logits GEMM (z = W h: A = LM-head rows, B = gathered hidden rows, K = d).
+// Eight wavefronts (two per SIMD, so one can issue MFMAs while the other waits on memory) each
+// own a 128 x 64 part of the block tile.  LDS holds two stages of a 256 x 64 A tile and a
+// 256 x 64 B tile (32 KB each), written by direct global->LDS loads (global_load_lds_dwordx4):
+// one load instruction moves 1 KB, lane l writing its 16-byte slot l; each wavefront moves
+// 4 KB of each operand per tile.  Tile kt+1 is in flight while tile kt is multiplied;
+// fragments of k-step kk+1 are read while the MFMAs of k-step kk run.  With K short (one
+// tile row spans d), this engine keeps more MFMA work in flight per block than the four-
+// wavefront engine of the backward GEMMs, and measured faster on the logits shape.
+//
+// LDS layout (rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
+// c ^ ((r >> 1) & 7).  The LDS serves a 16-byte-per-lane read 16 lanes (256 B, 64 banks) at a
+// time, and rows r..r+15 of a fragment then land on 16 distinct 16-byte bank groups; the
+// swizzle is applied on the global side (each lane loads the chunk that belongs in its slot).
+template <int MODE>
+__device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, int n0,
+                                                  f32x16_t (&acc)[4][2], uint16_t* smem) {
   constexpr int BK = 64;
   constexpr int TILE = kBM * BK;  // elements per operand per stage
   const int tid = threadIdx.x, lane = tid & 63;
@@ -199,27 +399,15 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = wave * 32 + j * 8 + lrow;
-    if (!A_KMAJOR) {
-      const int ra = min(m0 + r, p.M - 1);  // rows past the edge load a valid row; their
-      arow[j] = int64_t(ra) * p.lda;        // results are never stored
-    } else {
-      // K-major A: instruction j moves rows k = 2 (4 wave + j) + (lane >> 5) of the tile,
-      // 32 slots of 16 B each; slot (lane & 31) holds m-chunk (lane & 31) ^ ((k & 3) << 2)
-      const int kr = 2 * (wave * 4 + j) + (lane >> 5);
-      const int c = (lane & 31) ^ ((kr & 3) << 2);
-      arow[j] = int64_t(kr) * p.lda + m0 + c * 8;
-    }
-    const int rb = min(n0 + r, p.N - 1);
-    int64_t br = rb;
-    if (MODE == MODE_FWD) {
-      br += p.b_row_base;
-      if (p.b_rows) br = p.b_rows[br];
-    }
+    const int ra = min(m0 + r, p.M - 1);  // rows past the edge load a valid row; their
+    arow[j] = int64_t(ra) * p.lda;        // results are never stored
+    int64_t br = min(n0 + r, p.N - 1) + p.b_row_base;
+    if (p.b_rows) br = p.b_rows[br];
     brow[j] = br * p.ldb;
   }
   const int K = p.K;
   const int nk = (K + BK - 1) / BK;
-  const bool ktail = (K % BK) != 0;  // never true for K-major A (K is padded to 256)
+  const bool ktail = (K % BK) != 0;
   auto issue = [&](int kt, int stage) {
     // clamp the chunk so a partial last tile never reads past the end of a row
     const int kc0 = min(kt * BK + gch[0] * 8, K - 8);
@@ -229,12 +417,7 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int kc = (j & 1) ? kc1 : kc0;
-      if (A_KMAJOR)
-        __builtin_amdgcn_global_load_lds(Ag + arow[j] + int64_t(kt) * BK * p.lda,
-                                         (lds_void_t*)(sa + j * 8 * BK), 16, 0, 0);
-      else
-        __builtin_amdgcn_global_load_lds(Ag + arow[j] + kc, (lds_void_t*)(sa + j * 8 * BK), 16,
-                                         0, 0);
+      __builtin_amdgcn_global_load_lds(Ag + arow[j] + kc, (lds_void_t*)(sa + j * 8 * BK), 16, 0, 0);
       __builtin_amdgcn_global_load_lds(Bg + brow[j] + kc, (lds_void_t*)(sb + j * 8 * BK), 16, 0, 0);
     }
   };
@@ -249,52 +432,16 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     }
   };
   const int sw = (lane >> 1) & 7;  // ((row >> 1) & 7) of the fragment rows this lane reads
-  // K-major A fragment source: group g = lane / 16, i = lane % 16 reads row
-  // k = 8 (g / 2) + 4 s + i / 4 (s = first / second half of the 8 k), m = 16 (g % 2) + 4 (i % 4)
-  const int tg = lane >> 4, ti = lane & 15;
-  const int tr_k = 8 * (tg >> 1) + (ti >> 2);
-  const int tr_m = 16 * (tg & 1) + 4 * (ti & 3);
-  // A fragments i0 .. i1-1 of k-step kk
-  auto frags_a = [&](int stage, int kk, bf16x8_t (&fa)[4], int i0, int i1) {
+  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2]) {
     const uint16_t* as = smem + stage * 2 * TILE;
+    const uint16_t* bs = as + TILE;
     const int slot = ((kk * 2 + (lane >> 5)) ^ sw) * 8;
-    if (A_KMAJOR) {
 #pragma unroll
-      for (int i = i0; i < i1; ++i) {
-        const int m = wm * 128 + i * 32 + tr_m;
-        s16x4_t h[2];
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int k = kk * 16 + tr_k + 4 * hh;
-          const int c = (m >> 3) ^ ((k & 3) << 2);
-          // issued as asm: the compiler's wait analysis cannot tell this read from the
-          // in-flight DMA into the other stage and would wait on vmcnt; the step that uses
-          // the result waits explicitly (wait_a)
-          const uint32_t addr = uint32_t(uintptr_t(
-              (const __attribute__((address_space(3))) uint16_t*)(as + k * kBM + c * 8 + (m & 7))));
-          asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(h[hh]) : "v"(addr) : "memory");
-        }
-        const s16x4_t lo = h[0], hi = h[1];
-        typedef short s16x8_t __attribute__((ext_vector_type(8)));
-        const s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        fa[i] = __builtin_bit_cast(bf16x8_t, v);
-      }
-    } else {
-#pragma unroll
-      for (int i = i0; i < i1; ++i)
-        fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 32 + (lane & 31)) * BK + slot);
-    }
-  };
-  auto frags_b = [&](int stage, int kk, bf16x8_t (&fb)[2]) {
-    const uint16_t* bs = smem + stage * 2 * TILE + TILE;
-    const int slot = ((kk * 2 + (lane >> 5)) ^ sw) * 8;
+    for (int i = 0; i < 4; ++i)
+      fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 32 + (lane & 31)) * BK + slot);
 #pragma unroll
     for (int j = 0; j < 2; ++j)
       fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 64 + j * 32 + (lane & 31)) * BK + slot);
-  };
-  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2]) {
-    frags_a(stage, kk, fa, 0, 4);
-    frags_b(stage, kk, fb);
   };
   auto mma = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[2]) {
 #pragma unroll
@@ -310,59 +457,21 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
       for (int j = 0; j < 2; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
-  constexpr int NREAD = A_KMAJOR ? 2 : 6;  // compiler-visible LDS reads per k-step
-  // K-major A: the asm reads of a step's A fragments must land before its MFMAs; the wait
-  // is tied to the fragment registers so no MFMA using them can move above it
-  // (the B fragments are tied too, so the compiler's own wait for them lands here, before
-  // the next step's reads are issued, and not after them)
-  auto wait_a = [&](bf16x8_t (&fa)[4], bf16x8_t (&fb)[2]) {
-    if (A_KMAJOR)
-      asm volatile("s_waitcnt lgkmcnt(0)"
-                   : "+v"(fa[0]), "+v"(fa[1]), "+v"(fa[2]), "+v"(fa[3]), "+v"(fb[0]),
-                     "+v"(fb[1])::"memory");
-  };
-
-  auto mma_row = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[2], int i) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-  };
 
   bf16x8_t fa0[4], fb0[2], fa1[4], fb1[2];
-  // pin the order inside a k-step: the 8 MFMAs of this step with the fragment reads of
-  // the next step spread among them (at most one step's reads in flight, so the wait before
-  // the next step's MFMAs is exact, and the last read still has 4 MFMAs to land)
-#define FR_STEP_ORDER()                                              \
-  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                 \
-  __builtin_amdgcn_sched_group_barrier(0x100, (NREAD + 1) / 2, 0);   \
-  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                 \
-  __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);         \
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                 \
-  __builtin_amdgcn_sched_barrier(0)
-  // one full k-step: the MFMAs of step kk (fragments fa, fb) with the reads of step kk + 1
-  // (into na, nb) spread among them.  The transposing reads of K-major A are inline asm, which
-  // the scheduling groups do not place: they are pinned between the MFMAs of rows 0, 1, 2-3.
+  // pin the order inside a k-step: the 8 MFMAs of this step with the 6 fragment reads of the
+  // next step spread among them (at most one step's reads in flight, so the wait before the
+  // next step's MFMAs is exact, and the last read still has 4 MFMAs to land)
   auto kstep = [&](int stage, int kk_next, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2],
                    bf16x8_t (&na)[4], bf16x8_t (&nb)[2]) {
-    wait_a(fa, fb);
-    if (A_KMAJOR) {
-      frags_b(stage, kk_next, nb);
-      mma_row(fa, fb, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      frags_a(stage, kk_next, na, 0, 2);
-      __builtin_amdgcn_sched_barrier(0);
-      mma_row(fa, fb, 1);
-      __builtin_amdgcn_sched_barrier(0);
-      frags_a(stage, kk_next, na, 2, 4);
-      __builtin_amdgcn_sched_barrier(0);
-      mma_row(fa, fb, 2);
-      mma_row(fa, fb, 3);
-      __builtin_amdgcn_sched_barrier(0);
-    } else {
-      frags(stage, kk_next, na, nb);
-      mma(fa, fb);
-      FR_STEP_ORDER();
-    }
+    frags(stage, kk_next, na, nb);
+    mma(fa, fb);
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_barrier(0);
   };
   issue(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -378,7 +487,6 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     kstep(cur, 3, fa0, fb0, fa1, fb1);
     // last k-step: half of its MFMAs cover the barrier; the other half cover the next
     // tile's load issue and the first fragment reads of tile kt+1
-    wait_a(fa1, fb1);
     mma_half(fa1, fb1, 0);
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tile kt+1 is in LDS
@@ -394,9 +502,9 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, (NREAD + 1) / 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, NREAD / 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the re-load above has landed
@@ -405,10 +513,8 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     kstep(cur, 1, fa0, fb0, fa1, fb1);
     kstep(cur, 2, fa1, fb1, fa0, fb0);
     kstep(cur, 3, fa0, fb0, fa1, fb1);
-    wait_a(fa1, fb1);
     mma(fa1, fb1);
   }
-#undef FR_STEP_ORDER
 }
 
 // float32 main loop (small problems): register-staged loads into padded LDS rows.  With
@@ -420,7 +526,7 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
   using E = Eng<float>;
   constexpr int BK = E::BK, LD = E::LD, VEC = E::VEC;
   constexpr int VPR = BK / VEC;
-  constexpr int LOADS = kBM * VPR / Geo<float>::THREADS;
+  constexpr int LOADS = kBM * VPR / Geo<float, MODE>::THREADS;
   float* As = smem;
   float* Bs = smem + 2 * kBM * LD;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -433,7 +539,7 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
   int kofs[LOADS], srow[LOADS], akk[LOADS], am4[LOADS];
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
-    const int v = tid + j * Geo<float>::THREADS;
+    const int v = tid + j * Geo<float, MODE>::THREADS;
     const int row = v / VPR;
     kofs[j] = (v % VPR) * VEC;
     srow[j] = row;
@@ -510,13 +616,13 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
 template <typename T>
 struct SmemBytes;
 template <>
-struct SmemBytes<uint16_t> { static constexpr int value = 2 * 2 * kBM * 64 * 2; };
+struct SmemBytes<uint16_t> { static constexpr int value = 2 * 2 * kTileP * 2; };
 template <>
 struct SmemBytes<float> { static constexpr int value = 2 * 2 * kBM * Eng<float>::LD * 4; };
 
 template <typename T, int MODE>
-__global__ __launch_bounds__(Geo<T>::THREADS)
-__attribute__((amdgpu_waves_per_eu(Geo<T>::WPE, Geo<T>::WPE)))
+__global__ __launch_bounds__((Geo<T, MODE>::THREADS))
+__attribute__((amdgpu_waves_per_eu(Geo<T, MODE>::WPE, Geo<T, MODE>::WPE)))
 void lm_gemm_kernel(const GemmParams p) {
   __shared__ __attribute__((aligned(16))) char smem_raw[SmemBytes<T>::value];
   T* smem = reinterpret_cast<T*>(smem_raw);
@@ -524,16 +630,17 @@ void lm_gemm_kernel(const GemmParams p) {
   tile_coords(mb, nb, p.nmb, p.nnb);
   if (MODE == MODE_FWD && p.store_e == 2 && p.redo_blk[nb] == 0) return;
   const int m0 = mb * kBM, n0 = nb * kBN;
-  constexpr int NI = Geo<T>::NI, NT = Geo<T>::THREADS;
+  constexpr int NI = Geo<T, MODE>::NI, NT = Geo<T, MODE>::THREADS;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / Geo<T>::WAVES_N, wn = wave % Geo<T>::WAVES_N;
+  const int wm = wave / Geo<T, MODE>::WAVES_N, wn = wave % Geo<T, MODE>::WAVES_N;
 
   f32x16_t acc[4][NI];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = f32x16_t{};
-  if constexpr (sizeof(T) == 2) mainloop_bf16<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
+  if constexpr (sizeof(T) == 2 && MODE == MODE_FWD) mainloop_bf16_dma<MODE>(p, m0, n0, acc, smem);
+  else if constexpr (sizeof(T) == 2) mainloop_bf16<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
   else mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
 
   // ------------------------------------------------------------------ epilogues
@@ -550,25 +657,27 @@ void lm_gemm_kernel(const GemmParams p) {
     const bool rows_full = m0 + kBM <= Vr;  // every vocab row of this block exists
 #pragma unroll
     for (int ni = 0; ni < NI; ++ni) {
-      const int cl = acc_col<T>(wn, ni, lane);
+      const int cl = acc_col<T, MODE>(wn, ni, lane);
       const int t = n0 + cl;                 // slab token
       const bool tok_ok = t < p.N;
       const int y = tok_ok ? p.yslab[t] : -1;
       // columns past the slab store exp(z - inf) = 0
       const float s_t = tok_ok ? (p.shift ? p.shift[t] : 0.0f) : INFINITY;
-      float mx = -INFINITY;
-      if (rows_full) {
+      // four independent chains (one per 32-row group), combined at the end
+      float mxp[4];
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
+      for (int mi = 0; mi < 4; ++mi) {
+        mxp[mi] = -INFINITY;
+        if (rows_full) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[mi][ni][r]);
-      } else {
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
+          for (int r = 0; r < 16; ++r) mxp[mi] = fmaxf(mxp[mi], acc[mi][ni][r]);
+        } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            mx = (m0 + acc_row(wm, mi, r, lane) < Vr) ? fmaxf(mx, acc[mi][ni][r]) : mx;
+            mxp[mi] = (m0 + acc_row(wm, mi, r, lane) < Vr) ? fmaxf(mxp[mi], acc[mi][ni][r]) : mxp[mi];
+        }
       }
+      float mx = fmaxf(fmaxf(mxp[0], mxp[1]), fmaxf(mxp[2], mxp[3]));
       // the sampled token's logit: held by one lane half of one wavefront (rare per column)
       const int dy = y - m0 - wm * 128;
       if (dy >= 0 && dy < 128 && ((dy >> 2) & 1) == (lane >> 5)) {
@@ -583,7 +692,8 @@ void lm_gemm_kernel(const GemmParams p) {
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       if (lane < 32) xmax[wm * kBN + cl] = mx;
       if (rel) {
-        float ssum = 0.0f, zsum = 0.0f;  // sum exp(z - s_t), sum exp(z - s_t) z
+        // sum exp(z - s_t) and sum exp(z - s_t) z, one chain per 32-row group
+        float ssp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, zsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
         T* e1 = static_cast<T*>(p.E1) + int64_t(t) * p.ldE1;
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi) {
@@ -595,8 +705,8 @@ void lm_gemm_kernel(const GemmParams p) {
             for (int q = 0; q < 4; ++q) {
               e[q] = __expf(acc[mi][ni][rg * 4 + q] - s_t);
               if (!rows_full && m0 + acc_row(wm, mi, rg * 4 + q, lane) >= Vr) e[q] = 0.0f;
-              ssum += e[q];
-              zsum = fmaf(e[q], acc[mi][ni][rg * 4 + q], zsum);
+              ssp[mi] += e[q];
+              zsp[mi] = fmaf(e[q], acc[mi][ni][rg * 4 + q], zsp[mi]);
             }
             if constexpr (sizeof(T) == 2) {
               typedef float f32x2_t __attribute__((ext_vector_type(2)));
@@ -624,6 +734,8 @@ void lm_gemm_kernel(const GemmParams p) {
             *reinterpret_cast<uint4*>(e1 + v0 + 8) = make_uint4(P[2], P[3], Q[2], Q[3]);
           }
         }
+        float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
+        float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
         ssum += __shfl_xor(ssum, 32, 64);
         zsum += __shfl_xor(zsum, 32, 64);
         if (lane < 32) {
@@ -636,9 +748,9 @@ void lm_gemm_kernel(const GemmParams p) {
     if (!rel) {
 #pragma unroll
       for (int ni = 0; ni < NI; ++ni) {
-        const int cl = acc_col<T>(wn, ni, lane);
+        const int cl = acc_col<T, MODE>(wn, ni, lane);
         const float M = fmaxf(xmax[cl], xmax[kBN + cl]);
-        float ssum = 0.0f, zsum = 0.0f;
+        float ssp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, zsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
@@ -646,10 +758,12 @@ void lm_gemm_kernel(const GemmParams p) {
             const int v = m0 + acc_row(wm, mi, r, lane);
             if (v < Vr) {
               const float ex = __expf(acc[mi][ni][r] - M);
-              ssum += ex;
-              zsum = fmaf(ex, acc[mi][ni][r], zsum);
+              ssp[mi] += ex;
+              zsp[mi] = fmaf(ex, acc[mi][ni][r], zsp[mi]);
             }
           }
+        float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
+        float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
         ssum += __shfl_xor(ssum, 32, 64);
         zsum += __shfl_xor(zsum, 32, 64);
         if (lane < 32) {
@@ -679,7 +793,7 @@ void lm_gemm_kernel(const GemmParams p) {
           const float g = p.gslab[t], c = p.cslab[t];
 #pragma unroll
           for (int ni = 0; ni < NI; ++ni) {
-            const int n = n0 + acc_col<T>(wn, ni, lane);
+            const int n = n0 + acc_col<T, MODE>(wn, ni, lane);
             if (n < p.N) {
               const float wy = y >= 0 ? to_f32<T>(Wg[int64_t(y) * p.d + n]) : 0.0f;
               const float val = g * wy - c * acc[mi][ni][r];
@@ -709,13 +823,13 @@ void lm_gemm_kernel(const GemmParams p) {
             const T* hrow = Hg + row * p.d;
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) {
-              const int n = n0 + acc_col<T>(wn, ni, lane);
+              const int n = n0 + acc_col<T, MODE>(wn, ni, lane);
               oh[ni] += n < p.N ? gt * to_f32<T>(hrow[n]) : 0.0f;
             }
           }
 #pragma unroll
           for (int ni = 0; ni < NI; ++ni) {
-            const int n = n0 + acc_col<T>(wn, ni, lane);
+            const int n = n0 + acc_col<T, MODE>(wn, ni, lane);
             if (n < p.N) {
               const int64_t o = int64_t(v) * p.d + n;
               const float prev = p.dW_acc ? p.dW[o] : 0.0f;
@@ -1063,8 +1177,12 @@ static int launch_gemm(GemmParams p, int kind, double flops, hipStream_t stream)
   p.nnb = int((p.N + kBN - 1) / kBN);
   const int64_t nblk = int64_t(p.nmb) * p.nnb;
   if (nblk == 0) return FASTRL_OK;
+  FR_CHECK_ARG(sizeof(T) != 2 || MODE == MODE_FWD ||
+                   (p.K % 64 == 0 && p.lda < (int64_t(1) << 23) && p.ldb < (int64_t(1) << 23)),
+               FASTRL_ERR_UNSUPPORTED,
+               "backward GEMM: K must be a multiple of 64 and leading dimensions below 2^23");
   ProfScope prof(kind, stream, flops);
-  hipLaunchKernelGGL((lm_gemm_kernel<T, MODE>), dim3(unsigned(nblk)), dim3(Geo<T>::THREADS), 0,
+  hipLaunchKernelGGL((lm_gemm_kernel<T, MODE>), dim3(unsigned(nblk)), dim3(Geo<T, MODE>::THREADS), 0,
                      stream, p);
   FR_LAUNCHED();
   return FASTRL_OK;
