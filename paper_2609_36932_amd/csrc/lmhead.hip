@@ -111,14 +111,17 @@ struct GemmParams {
   int32_t* status;
 };
 
+// M-blocks per N sweep in the tile order of each GEMM
+constexpr int kGroupFwd = 4, kGroupDh = 4, kGroupDw = 1;
+template <int MODE>
 __device__ __forceinline__ void tile_coords(int& mb, int& nb, int nmb, int nnb) {
   const int nblk = gridDim.x;
   int b = blockIdx.x;
   // consecutive logical tiles on the same XCD (blocks are dealt round-robin to 8 XCDs)
   const int full = (nblk / 8) * 8;
   if (b < full) b = (b % 8) * (full / 8) + b / 8;
-  // grouped order: 4 M-blocks share each N-block sweep
-  constexpr int GROUP = 4;
+  // grouped order: GROUP M-blocks share each N-block sweep
+  constexpr int GROUP = MODE == 0 ? kGroupFwd : MODE == 1 ? kGroupDh : kGroupDw;
   const int per_group = GROUP * nnb;
   const int gid = b / per_group;
   const int first = gid * GROUP;
@@ -627,7 +630,7 @@ void lm_gemm_kernel(const GemmParams p) {
   __shared__ __attribute__((aligned(16))) char smem_raw[SmemBytes<T>::value];
   T* smem = reinterpret_cast<T*>(smem_raw);
   int mb, nb;
-  tile_coords(mb, nb, p.nmb, p.nnb);
+  tile_coords<MODE>(mb, nb, p.nmb, p.nnb);
   if (MODE == MODE_FWD && p.store_e == 2 && p.redo_blk[nb] == 0) return;
   const int m0 = mb * kBM, n0 = nb * kBN;
   constexpr int NI = Geo<T, MODE>::NI, NT = Geo<T, MODE>::THREADS;
