@@ -102,12 +102,7 @@ struct GemmParams {
   int32_t d;
   // ---- DW epilogue
   float* dW;                // [V, d]
-  int32_t dW_acc;
-  const int32_t* lab_off;   // [V+1]  slab tokens grouped by label
-  const int32_t* lab_tok;   // [slab]
-  const void* H;            // hidden
-  const int32_t* row_index; // nullable
-  int64_t row_base;         // first kept token of the slab
+  int32_t dW_acc;           // add to dW (later slabs) instead of overwriting it
   int32_t* status;
 };
 
@@ -808,37 +803,29 @@ void lm_gemm_kernel(const GemmParams p) {
           }
         }
       }
-  } else {  // MODE_DW
-    const T* Hg = static_cast<const T*>(p.H);
+  } else {  // MODE_DW: dW[v] (+)= -C[v]; the one-hot part is added by dw_onehot_kernel
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = m0 + acc_row(wm, mi, r, lane);
-        if (v < p.M) {
-          // onehot part: sum of g_t H[t] over the slab tokens labelled v (index order)
-          float oh[NI] = {};
-          const int b0 = p.lab_off[v], b1 = p.lab_off[v + 1];
-          for (int e = b0; e < b1; ++e) {
-            const int t = p.lab_tok[e];
-            int64_t row = p.row_base + t;
-            if (p.row_index) row = p.row_index[row];
-            const float gt = p.gslab[t];
-            const T* hrow = Hg + row * p.d;
+      for (int rh = 0; rh < 16; rh += 8) {
+        // every load of these 8 rows first, so that their latencies overlap
+        float prev[8][NI];
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) {
-              const int n = n0 + acc_col<T, MODE>(wn, ni, lane);
-              oh[ni] += n < p.N ? gt * to_f32<T>(hrow[n]) : 0.0f;
-            }
-          }
+        for (int r = 0; r < 8; ++r) {
+          const int v = m0 + acc_row(wm, mi, rh + r, lane);
 #pragma unroll
           for (int ni = 0; ni < NI; ++ni) {
             const int n = n0 + acc_col<T, MODE>(wn, ni, lane);
-            if (n < p.N) {
-              const int64_t o = int64_t(v) * p.d + n;
-              const float prev = p.dW_acc ? p.dW[o] : 0.0f;
-              p.dW[o] = prev + oh[ni] - acc[mi][ni][r];
-            }
+            prev[r][ni] = (p.dW_acc && v < p.M && n < p.N) ? p.dW[int64_t(v) * p.d + n] : 0.0f;
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const int v = m0 + acc_row(wm, mi, rh + r, lane);
+#pragma unroll
+          for (int ni = 0; ni < NI; ++ni) {
+            const int n = n0 + acc_col<T, MODE>(wn, ni, lane);
+            if (v < p.M && n < p.N) p.dW[int64_t(v) * p.d + n] = prev[r][ni] - acc[mi][ni][rh + r];
           }
         }
       }
@@ -1171,6 +1158,32 @@ __global__ void label_sort_kernel(const int32_t* __restrict__ off, int32_t V,
   }
 }
 
+// One-hot part of dW for one slab: dW[v] += sum over the slab tokens t labelled v of g_t H[t],
+// summed in the label CSR's fixed token order (deterministic).  One block per distinct label:
+// the block of the label's first CSR entry does the work, the others exit.
+template <typename T>
+__global__ __launch_bounds__(256) void dw_onehot_kernel(
+    const int32_t* __restrict__ lab_off, const int32_t* __restrict__ lab_tok,
+    const int32_t* __restrict__ yslab, const float* __restrict__ gslab, const T* __restrict__ H,
+    const int32_t* __restrict__ row_index, int64_t row_base, int32_t d, int32_t V,
+    float* __restrict__ dW) {
+  const int e = blockIdx.x;
+  if (e >= lab_off[V]) return;
+  const int y = yslab[lab_tok[e]];
+  const int a = lab_off[y], b = lab_off[y + 1];
+  if (a != e) return;
+  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+    float s = 0.0f;
+    for (int i = a; i < b; ++i) {
+      const int t = lab_tok[i];
+      int64_t row = row_base + t;
+      if (row_index) row = row_index[row];
+      s += gslab[t] * to_f32<T>(H[row * d + n]);
+    }
+    dW[int64_t(y) * d + n] += s;
+  }
+}
+
 // ------------------------------------------------------------------ host side
 
 static inline int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -1468,10 +1481,15 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
       q.B = w.Bd; q.ldb = tcp; q.N = d;
       q.K = int32_t(Tr);
       q.dW = a.dW; q.dW_acc = (si > 0 || a.dW_accumulate) ? 1 : 0;
-      q.lab_off = w.lab_off; q.lab_tok = w.lab_tok; q.gslab = w.gslab;
-      q.H = a.hidden; q.row_index = a.row_index; q.row_base = t0; q.d = d;
+      q.d = d;
       q.status = a.status;
       FR_TRY((launch_gemm<T, MODE_DW>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
+      if (Tc > 0) {
+        hipLaunchKernelGGL((dw_onehot_kernel<T>), dim3(unsigned(Tc)), dim3(256), 0, stream,
+                           w.lab_off, w.lab_tok, w.yslab, w.gslab, static_cast<const T*>(a.hidden),
+                           a.row_index, t0, d, V, a.dW);
+        FR_LAUNCHED();
+      }
     }
   }
   hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, stream, w.seq_loss, w.seq_clip,
