@@ -804,14 +804,16 @@ void lm_gemm_kernel(const GemmParams p) {
         }
       }
   } else {  // MODE_DW: dW[v] (+)= -C[v]; the one-hot part is added by dw_onehot_kernel
+    // RB rows at a time (fewer where the float32 engine leaves fewer free registers)
+    constexpr int RB = sizeof(T) == 2 ? 8 : 4;
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-      for (int rh = 0; rh < 16; rh += 8) {
-        // every load of these 8 rows first, so that their latencies overlap
-        float prev[8][NI];
+      for (int rh = 0; rh < 16; rh += RB) {
+        // every load of these rows first, so that their latencies overlap
+        float prev[RB][NI];
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
+        for (int r = 0; r < RB; ++r) {
           const int v = m0 + acc_row(wm, mi, rh + r, lane);
 #pragma unroll
           for (int ni = 0; ni < NI; ++ni) {
@@ -820,7 +822,7 @@ void lm_gemm_kernel(const GemmParams p) {
           }
         }
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
+        for (int r = 0; r < RB; ++r) {
           const int v = m0 + acc_row(wm, mi, rh + r, lane);
 #pragma unroll
           for (int ni = 0; ni < NI; ++ni) {
