@@ -1174,15 +1174,21 @@ __global__ __launch_bounds__(256) void dw_onehot_kernel(
   const int y = yslab[lab_tok[e]];
   const int a = lab_off[y], b = lab_off[y + 1];
   if (a != e) return;
-  for (int n = threadIdx.x; n < d; n += blockDim.x) {
-    float s = 0.0f;
+  // four consecutive columns per thread (d is a multiple of 8), their loads independent
+  for (int n0 = threadIdx.x * 4; n0 < d; n0 += blockDim.x * 4) {
+    float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int i = a; i < b; ++i) {
       const int t = lab_tok[i];
       int64_t row = row_base + t;
       if (row_index) row = row_index[row];
-      s += gslab[t] * to_f32<T>(H[row * d + n]);
+      const float g = gslab[t];
+      const T* h = H + row * d + n0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s[q] += g * to_f32<T>(h[q]);
     }
-    dW[int64_t(y) * d + n] += s;
+    float* w = dW + int64_t(y) * d + n0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] += s[q];
   }
 }
 
