@@ -208,7 +208,8 @@ int fastrl_prune_ex(const fastrl_prune_args* args, hipStream_t stream);
  *   lse[t]  = log sum_v exp(z[t, v])       (vocab-chunked online max / sum-exp)
  *   logp[t] = z[t, y_t] - lse[t],          y_t = token_ids[r_t]
  * The [T, V] logits are never stored.  hidden row r is the final hidden state whose LM-head
- * output scores token_ids[r].  d % 8 == 0, V >= 1, T >= 0; lse may be NULL.
+ * output scores token_ids[r].  d % 8 == 0, V >= 1, T >= 0; lse may be NULL.  hidden and W
+ * are read in 16-byte pieces: both must be 16-byte aligned (FASTRL_ERR_VALUE otherwise).
  * ------------------------------------------------------------------------------------ */
 size_t fastrl_token_logprob_workspace_size(int64_t T, int32_t d, int32_t V, int32_t dtype);
 int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const void* W,
@@ -246,7 +247,8 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
  *   training, Sec. 4), accumulated in the same pass as the log-sum-exp (one more partial
  *   sum exp(z - s_t) z per vocabulary block).  entropy_sum [1] float (may be NULL): sum_t H_t
  *   in float64, fixed order (the mean entropy is entropy_sum / T).
- * Limits: d % 8 == 0; S >= 0; every sequence no longer than the slab (slab_tokens, 0 picks
+ * Limits: d % 8 == 0; hidden and W 16-byte aligned (FASTRL_ERR_VALUE); S >= 0; every
+ *   sequence no longer than the slab (slab_tokens, 0 picks
  *   the default of 32768 tokens; a longer sequence raises the slab to its length).  The
  *   tokens are spread over ceil(T / slab_tokens) slabs of about equal size.
  * The work runs slab by slab; each slab stores exp(z - s_t) (s_t = 0, or the row max when

@@ -65,6 +65,7 @@ ProfScope::~ProfScope() {
 }
 
 static bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace fastrl
 
@@ -196,6 +197,8 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
   if (T == 0) return FASTRL_OK;
   FR_CHECK_ARG(hidden && W && token_ids && logp, FASTRL_ERR_NULL_PTR,
                "fastrl_token_logprob: hidden / W / token_ids / logp is NULL");
+  FR_CHECK_ARG(aligned16(hidden) && aligned16(W), FASTRL_ERR_VALUE,
+               "fastrl_token_logprob: hidden and W must be 16-byte aligned");
   const size_t need = token_logprob_workspace(T, d, V, dtype);
   FR_CHECK_ARG(ws && aligned256(ws) && ws_bytes >= need, FASTRL_ERR_WORKSPACE,
                "fastrl_token_logprob: workspace missing, misaligned or smaller than " +
@@ -230,9 +233,12 @@ static int check_loss_args(const fastrl_loss_args* a, bool need_ws) {
   for (int32_t i = 0; i < a->S; ++i)
     FR_CHECK_ARG(a->seq_off_host[i + 1] >= a->seq_off_host[i], FASTRL_ERR_SHAPE,
                  "fastrl_policy_loss: seq_off_host is not monotone");
-  if (a->T > 0)
+  if (a->T > 0) {
     FR_CHECK_ARG(a->hidden && a->W && a->token_ids && a->old_logp, FASTRL_ERR_NULL_PTR,
                  "fastrl_policy_loss: hidden / W / token_ids / old_logp is NULL");
+    FR_CHECK_ARG(aligned16(a->hidden) && aligned16(a->W), FASTRL_ERR_VALUE,
+                 "fastrl_policy_loss: hidden and W must be 16-byte aligned");
+  }
   FR_CHECK_ARG(a->S == 0 || a->adv, FASTRL_ERR_NULL_PTR, "fastrl_policy_loss: adv is NULL");
   FR_CHECK_ARG(a->beta == 0.0f || a->ref_logp || a->T == 0, FASTRL_ERR_NULL_PTR,
                "fastrl_policy_loss: ref_logp is NULL while beta != 0");

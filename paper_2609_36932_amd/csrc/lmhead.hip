@@ -1064,31 +1064,60 @@ __global__ void loss_final_kernel(const double* __restrict__ seq_loss,
   }
 }
 
-// out[c][r] = scale(r) * in[row(r)][c], zero for r in [R, Rpad): tiled transpose via LDS
+// out[c][r] = scale(r) * in[row(r)][c], zero for r in [R, Rpad): 64 x 64 tiles through LDS with
+// 16-byte global loads and stores (C is a multiple of 8, in 16-byte aligned, Rpad and ldo
+// multiples of 64, out 256-byte aligned)
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_scale_kernel(
     const T* __restrict__ in, const int32_t* __restrict__ row_index, int64_t row_base,
     int32_t R, int32_t Rpad, int32_t C, const float* __restrict__ scale, T* __restrict__ out,
     int64_t ldo) {
+  constexpr int VEC = 16 / sizeof(T);  // elements per 16-byte piece: 8 bf16 or 4 float
+  constexpr int LPR = 64 / VEC;        // threads per 64-element tile row
+  constexpr int RPP = 256 / LPR;       // tile rows per pass
   __shared__ float tile[64][65];
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int rr = ty; rr < 64; rr += 4) {
+  const int tid = threadIdx.x;
+  const int l = (tid % LPR) * VEC;
+  for (int rr = tid / LPR; rr < 64; rr += RPP) {
     const int r = r0 + rr;
-    float v = 0.0f;
-    if (r < R && c0 + tx < C) {
+    float v[VEC];
+    if (r < R && c0 + l < C) {
       int64_t row = row_base + r;
       if (row_index) row = row_index[row];
-      v = to_f32<T>(in[row * C + c0 + tx]);
-      if (scale) v *= scale[r];
+      const u32x4_t raw = *reinterpret_cast<const u32x4_t*>(in + row * C + c0 + l);
+      const float sc = scale ? scale[r] : 1.0f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if constexpr (sizeof(T) == 2) {
+          v[2 * q] = bf16_to_f32(uint16_t(raw[q] & 0xffffu)) * sc;
+          v[2 * q + 1] = bf16_to_f32(uint16_t(raw[q] >> 16)) * sc;
+        } else {
+          v[q] = __uint_as_float(raw[q]) * sc;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) v[q] = 0.0f;
     }
-    tile[rr][tx] = v;
+#pragma unroll
+    for (int q = 0; q < VEC; ++q) tile[rr][l + q] = v[q];
   }
   __syncthreads();
-  for (int cc = ty; cc < 64; cc += 4) {
+  for (int cc = tid / LPR; cc < 64; cc += RPP) {
     const int c = c0 + cc;
-    const int r = r0 + tx;
-    if (c < C && r < Rpad) out[int64_t(c) * ldo + r] = from_f32<T>(tile[tx][cc]);
+    if (c < C && r0 + l < Rpad) {
+      u32x4_t o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if constexpr (sizeof(T) == 2)
+          o[q] = uint32_t(f32_to_bf16(tile[l + 2 * q][cc])) |
+                 (uint32_t(f32_to_bf16(tile[l + 2 * q + 1][cc])) << 16);
+        else
+          o[q] = __float_as_uint(tile[l + q][cc]);
+      }
+      *reinterpret_cast<u32x4_t*>(out + int64_t(c) * ldo + r0 + l) = o;
+    }
   }
 }
 

@@ -112,6 +112,25 @@ def test_host_validation_errors(fr):
     assert L.fastrl_policy_loss_fwd_bwd(ctypes.byref(a), None) == -4
 
 
+def test_lm_head_operands_must_be_16_byte_aligned(fr):
+    """hidden and W are read in 16-byte pieces: a misaligned pointer is refused on the host."""
+    L = fr._lib
+    p, q = ctypes.c_void_p(256), ctypes.c_void_p(258)
+    assert L.fastrl_token_logprob(q, None, p, 1, 4, 16, 10, p, p, None, None, None, 0,
+                                  None) == -3
+    assert b"16-byte" in L.fastrl_last_error()
+    assert L.fastrl_token_logprob(p, None, q, 1, 4, 16, 10, p, p, None, None, None, 0,
+                                  None) == -3
+    off = (ctypes.c_int64 * 2)(0, 4)
+    a = fr.LossArgs()
+    a.dtype, a.d, a.V, a.S, a.T = 1, 16, 10, 1, 4
+    a.seq_off_host = ctypes.cast(off, ctypes.c_void_p)
+    a.seq_off = a.loss = a.token_ids = a.old_logp = a.adv = p
+    a.hidden, a.W = p, q
+    assert L.fastrl_policy_loss_fwd_bwd(ctypes.byref(a), None) == -3
+    assert b"16-byte" in L.fastrl_last_error()
+
+
 def test_workspace_queries(fr):
     L = fr._lib
     assert L.fastrl_prune_workspace_size(4, 32, 1000, 8, 1) >= 1000 * 8
