@@ -248,9 +248,10 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
  *   sum exp(z - s_t) z per vocabulary block).  entropy_sum [1] float (may be NULL): sum_t H_t
  *   in float64, fixed order (the mean entropy is entropy_sum / T).
  * Limits: d % 8 == 0; hidden and W 16-byte aligned (FASTRL_ERR_VALUE); S >= 0; every
- *   sequence no longer than the slab (slab_tokens, 0 picks
- *   the default of 32768 tokens; a longer sequence raises the slab to its length).  The
- *   tokens are spread over ceil(T / slab_tokens) slabs of about equal size.
+ *   sequence no longer than the slab (slab_tokens; 0 picks the largest slab whose exp-logit
+ *   buffer stays within 48 GiB, ~169K tokens at V = 152064 in bf16; a longer sequence raises
+ *   the slab to its length).  The tokens are spread over ceil(T / slab_tokens) slabs of about
+ *   equal size.
  * The work runs slab by slab; each slab stores exp(z - s_t) (s_t = 0, or the row max when
  * exp(z) would leave float range) for its tokens in the workspace, so the workspace holds
  * slab * V_pad * sizeof(dtype) bytes (V_pad = V rounded up to 256), W^T (d * V_pad) when

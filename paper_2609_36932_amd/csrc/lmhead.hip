@@ -1319,7 +1319,11 @@ int run_token_logprob(const void* hidden, const int32_t* row_index, const void* 
 }
 
 // ---------------------------------------------------------------- loss forward/backward
-constexpr int64_t kDefaultSlab = 32768;
+// Default slab: the largest whose exp-logit buffer [slab, V_pad] stays within 48 GiB of the
+// 288 GB of HBM (at V = 152064 in bf16, ~169K tokens); a caller bounds the workspace with
+// slab_tokens.  Fewer, larger slabs launch fewer GEMMs and skip the read-modify-write of dW
+// between slabs.
+constexpr int64_t kDefaultSlabBytes = int64_t(48) << 30;
 
 struct SlabPlan {
   std::vector<int32_t> seq_begin;  // first sequence of each slab; back() == S
@@ -1398,7 +1402,10 @@ static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_
 }
 
 static int64_t slab_cap(const fastrl_loss_args& a) {
-  return a.slab_tokens > 0 ? a.slab_tokens : kDefaultSlab;
+  if (a.slab_tokens > 0) return a.slab_tokens;
+  const int64_t esz = a.dtype == FASTRL_BF16 ? 2 : 4;
+  const int64_t cap = kDefaultSlabBytes / (rup(a.V, kBM) * esz);
+  return std::max<int64_t>(4096, cap / kBN * kBN);
 }
 
 size_t policy_loss_workspace(const fastrl_loss_args& a) {
