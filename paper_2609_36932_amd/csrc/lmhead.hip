@@ -34,6 +34,7 @@ namespace fastrl {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 256, kBN = 256;
@@ -372,7 +373,11 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // 256 x 64 B tile (32 KB each), written by direct global->LDS loads (global_load_lds_dwordx4):
 // one load instruction moves 1 KB, lane l writing its 16-byte slot l; each wavefront moves
 // 4 KB of each operand per tile.  Tile kt+1 is in flight while tile kt is multiplied;
-// fragments of k-step kk+1 are read while the MFMAs of k-step kk run.  With K short (one
+// fragments of k-step kk+1 are read while the MFMAs of k-step kk run.  The MFMAs are
+// v_mfma_f32_16x16x32_bf16 (8 x 4 tiles of 16 x 16 per wavefront, two 32-k steps per tile):
+// per FLOP they move less accumulator data through the register file than 32 x 32 x 16, and
+// on this kernel measured 6% faster; lane l holds rows 4 (l / 16) .. 4 (l / 16) + 3 of column
+// l % 16 of each 16 x 16 tile.  With K short (one
 // tile row spans d), this engine keeps more MFMA work in flight per block than the four-
 // wavefront engine of the backward GEMMs, and measured faster on the logits shape.
 //
@@ -382,7 +387,7 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // swizzle is applied on the global side (each lane loads the chunk that belongs in its slot).
 template <int MODE>
 __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, int n0,
-                                                  f32x16_t (&acc)[4][2], uint16_t* smem) {
+                                                  f32x4_t (&acc)[8][4], uint16_t* smem) {
   constexpr int BK = 64;
   constexpr int TILE = kBM * BK;  // elements per operand per stage
   const int tid = threadIdx.x, lane = tid & 63;
@@ -430,46 +435,49 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
       }
     }
   };
-  const int sw = (lane >> 1) & 7;  // ((row >> 1) & 7) of the fragment rows this lane reads
-  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2]) {
+  const int sw = ((lane & 15) >> 1) & 7;  // ((row >> 1) & 7) of the fragment rows this lane reads
+  // fragments of the 32-k step kk (0, 1): A rows wm*128 + i*16 + (lane & 15) and B rows
+  // wn*64 + j*16 + (lane & 15), k-chunk 4 kk + lane / 16 (8 consecutive k per lane)
+  auto frags = [&](int stage, int kk, bf16x8_t (&fa)[8], bf16x8_t (&fb)[4]) {
     const uint16_t* as = smem + stage * 2 * TILE;
     const uint16_t* bs = as + TILE;
-    const int slot = ((kk * 2 + (lane >> 5)) ^ sw) * 8;
+    const int slot = ((kk * 4 + (lane >> 4)) ^ sw) * 8;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 32 + (lane & 31)) * BK + slot);
+    for (int i = 0; i < 8; ++i)
+      fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 16 + (lane & 15)) * BK + slot);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 64 + j * 32 + (lane & 31)) * BK + slot);
+    for (int j = 0; j < 4; ++j)
+      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 64 + j * 16 + (lane & 15)) * BK + slot);
   };
-  auto mma = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[2]) {
+  auto mma = [&](const bf16x8_t (&fa)[8], const bf16x8_t (&fb)[4]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
-  auto mma_half = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[2], int h) {
+  auto mma_half = [&](const bf16x8_t (&fa)[8], const bf16x8_t (&fb)[4], int h) {
 #pragma unroll
-    for (int i = 2 * h; i < 2 * h + 2; ++i)
+    for (int i = 4 * h; i < 4 * h + 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
 
-  bf16x8_t fa0[4], fb0[2], fa1[4], fb1[2];
-  // pin the order inside a k-step: the 8 MFMAs of this step with the 6 fragment reads of the
-  // next step spread among them (at most one step's reads in flight, so the wait before the
-  // next step's MFMAs is exact, and the last read still has 4 MFMAs to land)
-  auto kstep = [&](int stage, int kk_next, bf16x8_t (&fa)[4], bf16x8_t (&fb)[2],
-                   bf16x8_t (&na)[4], bf16x8_t (&nb)[2]) {
+  bf16x8_t fa0[8], fb0[4], fa1[8], fb1[4];
+  // pin the order inside a k-step: the 32 MFMAs of this step with the 12 fragment reads of the
+  // next step spread among the first 24 (at most one step's reads in flight, so the wait before
+  // the next step's MFMAs is exact, and the last read still has 8 MFMAs to land)
+  auto kstep = [&](int stage, int kk_next, bf16x8_t (&fa)[8], bf16x8_t (&fb)[4],
+                   bf16x8_t (&na)[8], bf16x8_t (&nb)[4]) {
     frags(stage, kk_next, na, nb);
     mma(fa, fb);
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+#pragma unroll
+    for (int q = 0; q < 12; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     __builtin_amdgcn_sched_barrier(0);
   };
   issue(0, 0);
@@ -482,8 +490,6 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
   for (; kt + 1 < nk; ++kt) {
     const int cur = kt & 1;
     kstep(cur, 1, fa0, fb0, fa1, fb1);
-    kstep(cur, 2, fa1, fb1, fa0, fb0);
-    kstep(cur, 3, fa0, fb0, fa1, fb1);
     // last k-step: half of its MFMAs cover the barrier; the other half cover the next
     // tile's load issue and the first fragment reads of tile kt+1
     mma_half(fa1, fb1, 0);
@@ -501,17 +507,15 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the re-load above has landed
   {  // last tile
     const int cur = kt & 1;
     kstep(cur, 1, fa0, fb0, fa1, fb1);
-    kstep(cur, 2, fa1, fb1, fa0, fb0);
-    kstep(cur, 3, fa0, fb0, fa1, fb1);
     mma(fa1, fb1);
   }
 }
@@ -612,6 +616,145 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
   }
 }
 
+
+// Epilogue of the bf16 logits GEMM (16 x 16 accumulator tiles: acc[i][j] covers vocab rows
+// wm*128 + 16 i .. +15 and tokens wn*64 + 16 j .. +15; lane l holds rows 4 (l / 16) + q of
+// token column l % 16).  Per token column: the block's max over its vocab rows, the sampled
+// token's logit, and with a stored exp (store_e != 0) E[t][v] = exp(z - s_t) with the sums
+// sum exp(z - s_t) and sum exp(z - s_t) z; without one (old / ref log-probs), the sums relative
+// to the block max.  A column's 256 rows are spread over the 4 lane groups of two wavefronts:
+// lane shuffles, then one LDS exchange between the wavefronts.
+__device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, int n0, int mb,
+                                                  f32x4_t (&acc)[8][4], uint16_t* smem) {
+  __syncthreads();  // LDS operand buffers are reused for the cross-wave exchange
+  float* xmax = reinterpret_cast<float*>(smem);  // [2 wm][256 cols]
+  float* xsum = xmax + 2 * kBN;
+  float* xsz = xsum + 2 * kBN;
+  constexpr int NT = Geo<uint16_t, MODE_FWD>::THREADS;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int g = lane >> 4, c = lane & 15;
+  const int Vr = p.Vreal;
+  const bool rel = p.store_e != 0;
+  const bool rows_full = m0 + kBM <= Vr;  // every vocab row of this block exists
+  const int rbase = m0 + wm * 128 + 4 * g;  // vocab row of acc[i][j][q]: rbase + 16 i + q
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int cl = wn * 64 + j * 16 + c;
+    const int t = n0 + cl;  // slab token
+    const bool tok_ok = t < p.N;
+    const int y = tok_ok ? p.yslab[t] : -1;
+    // columns past the slab store exp(z - inf) = 0
+    const float s_t = tok_ok ? (p.shift ? p.shift[t] : 0.0f) : INFINITY;
+    // max over the lane's 32 rows in four independent chains
+    float mxp[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float z = acc[i][j][q];
+        mxp[i & 3] = (rows_full || rbase + 16 * i + q < Vr) ? fmaxf(mxp[i & 3], z) : mxp[i & 3];
+      }
+    float mx = fmaxf(fmaxf(mxp[0], mxp[1]), fmaxf(mxp[2], mxp[3]));
+    // the sampled token's logit: held by one lane group of one wavefront (rare per column)
+    const int dy = y - m0 - wm * 128;
+    if (dy >= 0 && dy < 128 && ((dy >> 2) & 3) == g) {
+      float zl = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) zl = (16 * i + q == (dy & ~12)) ? acc[i][j][q] : zl;
+      p.zlab[t] = zl;
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    if (g == 0) xmax[wm * kBN + cl] = mx;
+    if (rel) {
+      float ssp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, zsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      uint16_t* e1 = static_cast<uint16_t*>(p.E1) + int64_t(t) * p.ldE1;
+#pragma unroll
+      for (int ip = 0; ip < 4; ++ip) {  // tile pair 2 ip, 2 ip + 1
+        uint32_t pk[2][2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int i = 2 * ip + h;
+          float e[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            e[q] = __expf(acc[i][j][q] - s_t);
+            if (!rows_full && rbase + 16 * i + q >= Vr) e[q] = 0.0f;
+            ssp[ip] += e[q];
+            zsp[ip] = fmaf(e[q], acc[i][j][q], zsp[ip]);
+          }
+          typedef float f32x2_t __attribute__((ext_vector_type(2)));
+          typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+          pk[h][0] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[0], e[1]}, bf16x2_t));
+          pk[h][1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[2], e[3]}, bf16x2_t));
+        }
+        // lane group g holds rows 4 g .. 4 g + 3 of both tiles; one swap between the groups of
+        // each 32-lane half (odd group's tile-2ip rows <-> even group's tile-2ip+1 rows) leaves
+        // group g with 8 consecutive rows: tile 2 ip + (g & 1), rows 8 (g >> 1) .. + 7
+#pragma unroll
+        for (int w = 0; w < 2; ++w) {
+          const auto sw = __builtin_amdgcn_permlane16_swap(pk[0][w], pk[1][w], false, false);
+          pk[0][w] = sw[0];
+          pk[1][w] = sw[1];
+        }
+        const int v0 = m0 + wm * 128 + (2 * ip + (g & 1)) * 16 + (g >> 1) * 8;
+        *reinterpret_cast<uint4*>(e1 + v0) = make_uint4(pk[0][0], pk[0][1], pk[1][0], pk[1][1]);
+      }
+      float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
+      float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
+      ssum += __shfl_xor(ssum, 16, 64);
+      zsum += __shfl_xor(zsum, 16, 64);
+      ssum += __shfl_xor(ssum, 32, 64);
+      zsum += __shfl_xor(zsum, 32, 64);
+      if (g == 0) {
+        xsum[wm * kBN + cl] = ssum;
+        xsz[wm * kBN + cl] = zsum;
+      }
+    }
+  }
+  __syncthreads();
+  if (!rel) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int cl = wn * 64 + j * 16 + c;
+      const float M = fmaxf(xmax[cl], xmax[kBN + cl]);
+      float ssp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, zsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (rbase + 16 * i + q < Vr) {
+            const float ex = __expf(acc[i][j][q] - M);
+            ssp[i & 3] += ex;
+            zsp[i & 3] = fmaf(ex, acc[i][j][q], zsp[i & 3]);
+          }
+        }
+      float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
+      float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
+      ssum += __shfl_xor(ssum, 16, 64);
+      zsum += __shfl_xor(zsum, 16, 64);
+      ssum += __shfl_xor(ssum, 32, 64);
+      zsum += __shfl_xor(zsum, 32, 64);
+      if (g == 0) {
+        xsum[wm * kBN + cl] = ssum;
+        xsz[wm * kBN + cl] = zsum;
+      }
+    }
+    __syncthreads();
+  }
+  for (int cl = tid; cl < kBN; cl += NT) {
+    const int t = n0 + cl;
+    if (t < p.N) {
+      p.pmax[int64_t(mb) * p.ldp + t] = fmaxf(xmax[cl], xmax[kBN + cl]);
+      p.psum[int64_t(mb) * p.ldp + t] = xsum[cl] + xsum[kBN + cl];
+      if (p.psz) p.psz[int64_t(mb) * p.ldp + t] = xsz[cl] + xsz[kBN + cl];
+    }
+  }
+}
+
 template <typename T>
 struct SmemBytes;
 template <>
@@ -633,17 +776,28 @@ void lm_gemm_kernel(const GemmParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / Geo<T, MODE>::WAVES_N, wn = wave % Geo<T, MODE>::WAVES_N;
 
+  if constexpr (sizeof(T) == 2 && MODE == MODE_FWD) {
+    f32x4_t acc16[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc16[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    mainloop_bf16_dma<MODE>(p, m0, n0, acc16, smem);
+    fwd_epilogue_bf16(p, m0, n0, mb, acc16, smem);
+    return;
+  }
   f32x16_t acc[4][NI];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = f32x16_t{};
-  if constexpr (sizeof(T) == 2 && MODE == MODE_FWD) mainloop_bf16_dma<MODE>(p, m0, n0, acc, smem);
-  else if constexpr (sizeof(T) == 2) mainloop_bf16<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
-  else mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
+  if constexpr (sizeof(T) == 2 && MODE != MODE_FWD)
+    mainloop_bf16<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
+  else if constexpr (sizeof(T) == 4)
+    mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
 
   // ------------------------------------------------------------------ epilogues
-  if constexpr (MODE == MODE_FWD) {
+  if constexpr (MODE == MODE_FWD && sizeof(T) == 4) {  // float32 logits (bf16: fwd_epilogue_bf16)
     __syncthreads();  // LDS operand buffers are reused for the cross-wave exchange
     float* xmax = reinterpret_cast<float*>(smem);      // [2 wm][256 cols]
     float* xsum = xmax + 2 * kBN;
@@ -696,7 +850,6 @@ void lm_gemm_kernel(const GemmParams p) {
         T* e1 = static_cast<T*>(p.E1) + int64_t(t) * p.ldE1;
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi) {
-          uint32_t pk[8];  // bf16 pairs of the lane's 4-row groups rg = 0..3
 #pragma unroll
           for (int rg = 0; rg < 4; ++rg) {
             float e[4];
@@ -707,30 +860,8 @@ void lm_gemm_kernel(const GemmParams p) {
               ssp[mi] += e[q];
               zsp[mi] = fmaf(e[q], acc[mi][ni][rg * 4 + q], zsp[mi]);
             }
-            if constexpr (sizeof(T) == 2) {
-              typedef float f32x2_t __attribute__((ext_vector_type(2)));
-              typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-              pk[2 * rg] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[0], e[1]}, bf16x2_t));
-              pk[2 * rg + 1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[2], e[3]}, bf16x2_t));
-            } else {
-              const int v0 = m0 + acc_row(wm, mi, rg * 4, lane);
-              *reinterpret_cast<float4*>(e1 + v0) = make_float4(e[0], e[1], e[2], e[3]);
-            }
-          }
-          if constexpr (sizeof(T) == 2) {
-            // lane half h holds rows 8 rg + 4 h + 0..3 of this 32-row block; one swap of the
-            // halves' groups (rg 0,1 of the upper half <-> rg 2,3 of the lower half) leaves
-            // lane half h with the 16 consecutive rows 16 h .. 16 h + 15: two 16-byte stores
-            uint32_t P[4] = {pk[0], pk[1], pk[2], pk[3]}, Q[4] = {pk[4], pk[5], pk[6], pk[7]};
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-              const auto sw2 = __builtin_amdgcn_permlane32_swap(P[k], Q[k], false, false);
-              P[k] = sw2[0];
-              Q[k] = sw2[1];
-            }
-            const int v0 = m0 + wm * 128 + mi * 32 + (lane >> 5) * 16;
-            *reinterpret_cast<uint4*>(e1 + v0) = make_uint4(P[0], P[1], Q[0], Q[1]);
-            *reinterpret_cast<uint4*>(e1 + v0 + 8) = make_uint4(P[2], P[3], Q[2], Q[3]);
+            const int v0 = m0 + acc_row(wm, mi, rg * 4, lane);
+            *reinterpret_cast<float4*>(e1 + v0) = make_float4(e[0], e[1], e[2], e[3]);
           }
         }
         float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
