@@ -43,9 +43,11 @@ enum GemmMode { MODE_FWD = 0, MODE_DH = 1, MODE_DW = 2 };
 
 // wavefront geometry of the 256 x 256 block tile: the bf16 logits GEMM runs 8 wavefronts
 // (two per SIMD) of 128 x 64, every other GEMM 4 wavefronts of 128 x 128
+// GEMMs on the 8-wavefront engine (16 x 16 x 32 MFMAs, direct-to-LDS loads)
+constexpr bool kDh8 = true;
 template <typename T, int MODE>
 struct Geo {
-  static constexpr bool W8 = sizeof(T) == 2 && MODE == MODE_FWD;
+  static constexpr bool W8 = sizeof(T) == 2 && (MODE == MODE_FWD || (MODE == MODE_DH && kDh8));
   static constexpr int THREADS = W8 ? 512 : 256, WAVES_N = W8 ? 4 : 2, NI = W8 ? 2 : 4,
                        WPE = W8 ? 2 : 1;
 };
@@ -755,6 +757,38 @@ __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, i
   }
 }
 
+
+// Epilogue of the bf16 dhidden GEMM on the 16 x 16 layout (acc[i][j]: token rows wm*128 + 16 i
+// + 4 (l / 16) + q, hidden columns wn*64 + 16 j + l % 16): dH[t] = g_t W[y_t] - c_t C[t].
+__device__ __forceinline__ void dh_epilogue_bf16(const GemmParams& p, int m0, int n0,
+                                                 f32x4_t (&acc)[8][4]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int g = lane >> 4, c = lane & 15;
+  const uint16_t* Wg = static_cast<const uint16_t*>(p.W);
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int t = m0 + wm * 128 + 16 * i + 4 * g + q;
+      if (t < p.M) {
+        const int y = p.yslab[t];
+        const float gt = p.gslab[t], ct = p.cslab[t];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = n0 + wn * 64 + 16 * j + c;
+          if (n < p.N) {
+            const float wy = y >= 0 ? bf16_to_f32(Wg[int64_t(y) * p.d + n]) : 0.0f;
+            const float val = gt * wy - ct * acc[i][j][q];
+            const int64_t o = int64_t(t) * p.d + n;
+            if (p.dH_bf16) static_cast<uint16_t*>(p.dH)[o] = f32_to_bf16(val);
+            else static_cast<float*>(p.dH)[o] = val;
+          }
+        }
+      }
+    }
+}
+
 template <typename T>
 struct SmemBytes;
 template <>
@@ -776,14 +810,15 @@ void lm_gemm_kernel(const GemmParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / Geo<T, MODE>::WAVES_N, wn = wave % Geo<T, MODE>::WAVES_N;
 
-  if constexpr (sizeof(T) == 2 && MODE == MODE_FWD) {
+  if constexpr (Geo<T, MODE>::W8) {
     f32x4_t acc16[8][4];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc16[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
     mainloop_bf16_dma<MODE>(p, m0, n0, acc16, smem);
-    fwd_epilogue_bf16(p, m0, n0, mb, acc16, smem);
+    if constexpr (MODE == MODE_FWD) fwd_epilogue_bf16(p, m0, n0, mb, acc16, smem);
+    else dh_epilogue_bf16(p, m0, n0, acc16);
     return;
   }
   f32x16_t acc[4][NI];
@@ -791,7 +826,7 @@ void lm_gemm_kernel(const GemmParams p) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = f32x16_t{};
-  if constexpr (sizeof(T) == 2 && MODE != MODE_FWD)
+  if constexpr (sizeof(T) == 2 && !Geo<T, MODE>::W8)
     mainloop_bf16<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
   else if constexpr (sizeof(T) == 4)
     mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
@@ -911,7 +946,7 @@ void lm_gemm_kernel(const GemmParams p) {
         if (p.psz) p.psz[int64_t(mb) * p.ldp + t] = xsz[cl] + xsz[kBN + cl];
       }
     }
-  } else if constexpr (MODE == MODE_DH) {
+  } else if constexpr (MODE == MODE_DH && !Geo<T, MODE>::W8) {
     const T* Wg = static_cast<const T*>(p.W);
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
