@@ -41,13 +41,12 @@ constexpr int kBM = 256, kBN = 256;
 
 enum GemmMode { MODE_FWD = 0, MODE_DH = 1, MODE_DW = 2 };
 
-// wavefront geometry of the 256 x 256 block tile: the bf16 logits GEMM runs 8 wavefronts
-// (two per SIMD) of 128 x 64, every other GEMM 4 wavefronts of 128 x 128
-// GEMMs on the 8-wavefront engine (16 x 16 x 32 MFMAs, direct-to-LDS loads)
-constexpr bool kDh8 = true;
+// wavefront geometry of the 256 x 256 block tile: the bf16 logits and dhidden GEMMs run 8
+// wavefronts (two per SIMD) of 128 x 64 on 16 x 16 x 32 MFMAs; the bf16 dW GEMM and every
+// float32 GEMM run 4 wavefronts of 128 x 128 on 32 x 32 MFMAs
 template <typename T, int MODE>
 struct Geo {
-  static constexpr bool W8 = sizeof(T) == 2 && (MODE == MODE_FWD || (MODE == MODE_DH && kDh8));
+  static constexpr bool W8 = sizeof(T) == 2 && MODE != MODE_DW;
   static constexpr int THREADS = W8 ? 512 : 256, WAVES_N = W8 ? 4 : 2, NI = W8 ? 2 : 4,
                        WPE = W8 ? 2 : 1;
 };
@@ -162,7 +161,9 @@ __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
-// bf16 main loop of the backward GEMMs.  Four wavefronts (one per SIMD) each own a 128 x 128 part of the block tile.
+// bf16 main loop of the dW GEMM (dW = E^T Bd^T: A = the slab's exp-logit tile E read K-major,
+// B = the scaled hidden rows Bd).  Four wavefronts (one per SIMD) each own a 128 x 128 part of
+// the block tile.
 // Operand tiles of 64 k move global -> registers -> LDS through two register sets and two LDS
 // stages (a 256 x 64 A tile and a 256 x 64 B tile, 64 KB per stage).  Iteration kt:
 //   k-steps 0-1  MFMAs of tile kt; loads of tile kt+2 into register set kt % 2
@@ -175,23 +176,22 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 // MFMAs are interleaved with the next k-step's 8 fragment reads and the step's loads or LDS
 // writes.
 //
-// K-contiguous operand (rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
+// B (K-contiguous, rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
 // c ^ ((r >> 1) & 7).  A fragment read (16 lanes = 16 rows of one chunk per LDS cycle) lands on
 // 16 distinct 16-byte bank groups, and a staging write covers whole rows (8 lanes per row).
 //
-// K-major A (A_KMAJOR: A[m][k] stored at k * lda + m, i.e. the logits-exp tile E[t][v] read
-// as E^T for dW): the tile is 64 rows of k x 256 m (512 B), row k keeping its m-chunk c in
-// slot c ^ ((k & 3) << 2).  Fragments come from ds_read_b64_tr_b16: inside each 16-lane group,
+// A (K-major: A[m][k] stored at k * lda + m, the exp tile E[t][v] read as E^T): the tile is 64
+// rows of k x 256 m (512 B), row k keeping its m-chunk c in slot c ^ ((k & 3) << 2).  Fragments come from ds_read_b64_tr_b16: inside each 16-lane group,
 // source lane j reads 4 consecutive m of row kbase + j/4 at m = mbase + 4 (j % 4), and lane i
 // receives A[mbase + i][kbase .. kbase + 3] -- 4 consecutive k of one row m, as the MFMA wants.
 constexpr int kTileP = kBM * 64;  // elements per operand per stage
 
-// K is a multiple of 64 (the backward GEMMs run over the padded vocabulary or slab), and the
-// leading dimensions stay below 8M elements (checked at launch).
-template <int MODE, bool A_KMAJOR>
-__device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n0,
-                                              f32x16_t (&acc)[4][4], uint16_t* smem) {
-  static_assert(MODE != MODE_FWD, "the logits GEMM runs the 8-wavefront engine");
+// K is a multiple of 64 (the padded slab), and the leading dimensions stay below 8M elements
+// (checked at launch).
+template <int MODE>
+__device__ __forceinline__ void mainloop_bf16_dw(const GemmParams& p, int m0, int n0,
+                                                 f32x16_t (&acc)[4][4], uint16_t* smem) {
+  static_assert(MODE == MODE_DW, "the logits and dhidden GEMMs run the 8-wavefront engine");
   constexpr int BK = 64;
   constexpr int TILE = kTileP;
   constexpr int STAGE = 2 * TILE;
@@ -201,14 +201,11 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   const int K = p.K;
   const int nk = (K + BK - 1) / BK;
 
-  // staging: load j (0..7) of a K-contiguous operand moves row 32 j + tid / 8, k-chunk tid % 8;
-  // of the K-major A, k row 8 j + tid / 32, m-chunk tid % 32.  Row addresses are 32-bit element
-  // offsets from a per-block base (a block spans 256 rows), except the gathered rows of the
-  // logits' B operand, which keep full pointers.
+  // staging: load j (0..7) of B moves row 32 j + tid / 8, k-chunk tid % 8; of A, k row
+  // 8 j + tid / 32, m-chunk tid % 32.  Addresses are 32-bit byte offsets from a per-block base.
   const int srow = tid >> 3, sch = tid & 7;
   const int krow = tid >> 5, mch = tid & 31;
-  const char* Ab = reinterpret_cast<const char*>(static_cast<const uint16_t*>(p.A) +
-                                                 (A_KMAJOR ? int64_t(m0) : int64_t(m0) * p.lda));
+  const char* Ab = reinterpret_cast<const char*>(static_cast<const uint16_t*>(p.A) + m0);
   const char* Bb = reinterpret_cast<const char*>(static_cast<const uint16_t*>(p.B) +
                                                  int64_t(n0) * p.ldb);
   // byte offsets of this lane's 16-byte chunks from the tile base (below 2^32 for any
@@ -217,12 +214,11 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int r = 32 * j + srow;
+    ao[j] = (uint32_t(krow + 8 * j) * uint32_t(p.lda) + mch * 8) * 2;
     // rows past the edge load a valid row; their results are never stored
-    ao[j] = A_KMAJOR ? (uint32_t(krow + 8 * j) * uint32_t(p.lda) + mch * 8) * 2
-                     : (uint32_t(min(r, p.M - 1 - m0)) * uint32_t(p.lda) + sch * 8) * 2;
     bo[j] = (uint32_t(min(r, p.N - 1 - n0)) * uint32_t(p.ldb) + sch * 8) * 2;
   }
-  const int64_t a_tile = A_KMAJOR ? int64_t(BK) * p.lda * 2 : BK * 2;  // bytes per k-tile
+  const int64_t a_tile = int64_t(BK) * p.lda * 2;  // bytes per k-tile of A
 
   // loads j = 4 h .. 4 h + 3 of tile kt
   auto load_half = [&](int kt, int h, u32x4_t (&ra)[8], u32x4_t (&rb)[8]) {
@@ -243,12 +239,12 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
     uint16_t* sb = sa + TILE;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      *reinterpret_cast<u32x4_t*>(sa + (A_KMAJOR ? wkm + j * 8 * kBM : wk + j * WJ)) = ra[j];
+      *reinterpret_cast<u32x4_t*>(sa + wkm + j * 8 * kBM) = ra[j];
       *reinterpret_cast<u32x4_t*>(sb + wk + j * WJ) = rb[j];
     }
   };
 
-  // K-major A fragment source: group g = lane / 16, i = lane % 16 reads row
+  // A fragment source: group g = lane / 16, i = lane % 16 reads row
   // k = 8 (g / 2) + 4 s + i / 4 (s = first / second half of the 8 k), m = 16 (g % 2) + 4 (i % 4)
   const int tg = lane >> 4, ti = lane & 15;
   const int tr_k = 8 * (tg >> 1) + (ti >> 2);
@@ -257,31 +253,26 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
   auto read_frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[4]) {
     const uint16_t* as = smem + stage * STAGE;
     const uint16_t* bs = as + TILE;
-    // row (lane & 31) of a 32-row block, half lane / 32, of sub-tile kk
+    // B: row (lane & 31) of a 32-row block, k-chunk 2 kk + lane / 32
     const int fo = (lane & 31) * BK + ((kk * 2 + (lane >> 5)) ^ ((lane >> 1) & 7)) * 8;
-    constexpr int RS = BK;  // row stride
     auto read_a = [&](int i) {
-      if (A_KMAJOR) {
-        const int m = wm * 128 + i * 32 + tr_m;
-        s16x4_t h[2];
+      const int m = wm * 128 + i * 32 + tr_m;
+      s16x4_t h[2];
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int k = kk * 16 + tr_k + 4 * hh;
-          const int c = (m >> 3) ^ ((k & 3) << 2);
-          h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_s16x4_t*)(as + k * kBM + c * 8 + (m & 7)));
-        }
-        typedef short s16x8_t __attribute__((ext_vector_type(8)));
-        const s16x8_t v = {h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
-        fa[i] = __builtin_bit_cast(bf16x8_t, v);
-      } else {
-        fa[i] = *reinterpret_cast<const bf16x8_t*>(as + fo + (wm * 128 + i * 32) * RS);
+      for (int hh = 0; hh < 2; ++hh) {
+        const int k = kk * 16 + tr_k + 4 * hh;
+        const int c = (m >> 3) ^ ((k & 3) << 2);
+        h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4_t*)(as + k * kBM + c * 8 + (m & 7)));
       }
+      typedef short s16x8_t __attribute__((ext_vector_type(8)));
+      const s16x8_t v = {h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
+      fa[i] = __builtin_bit_cast(bf16x8_t, v);
     };
     read_a(0);
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + fo + (wn * 128 + j * 32) * RS);
+      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + fo + (wn * 128 + j * 32) * BK);
 #pragma unroll
     for (int i = 1; i < 4; ++i) read_a(i);
   };
@@ -292,8 +283,8 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
-  // fragment reads of one k-step (8, or 12 with the transposing A reads)
-  constexpr int NFR = A_KMAJOR ? 12 : 8;
+  // fragment reads of one k-step: 8 transposing A reads and 4 B reads
+  constexpr int NFR = 12;
   constexpr int NFR_SLOT = (NFR + 7) / 8;  // reads per interleave slot (8 slots per k-step)
 
   // one k-step's order: the next k-step's fragment reads and `n` instructions of class `mask`
@@ -369,7 +360,8 @@ __device__ __forceinline__ void mainloop_bf16(const GemmParams& p, int m0, int n
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// bf16 main loop of the logits GEMM (z = W h: A = LM-head rows, B = gathered hidden rows, K = d).
+// bf16 main loop of the logits GEMM (z = W h: A = LM-head rows, B = gathered hidden rows, K = d)
+// and of the dhidden GEMM (A = the slab's exp-logit rows, B = W^T rows, K = padded vocab).
 // Eight wavefronts (two per SIMD, so one can issue MFMAs while the other waits on memory) each
 // own a 128 x 64 part of the block tile.  LDS holds two stages of a 256 x 64 A tile and a
 // 256 x 64 B tile (32 KB each), written by direct global->LDS loads (global_load_lds_dwordx4):
@@ -378,10 +370,9 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // fragments of k-step kk+1 are read while the MFMAs of k-step kk run.  The MFMAs are
 // v_mfma_f32_16x16x32_bf16 (8 x 4 tiles of 16 x 16 per wavefront, two 32-k steps per tile):
 // per FLOP they move less accumulator data through the register file than 32 x 32 x 16, and
-// on this kernel measured 6% faster; lane l holds rows 4 (l / 16) .. 4 (l / 16) + 3 of column
-// l % 16 of each 16 x 16 tile.  With K short (one
-// tile row spans d), this engine keeps more MFMA work in flight per block than the four-
-// wavefront engine of the backward GEMMs, and measured faster on the logits shape.
+// measured 7% faster on the logits GEMM and 4% on dhidden (where this engine also beat the
+// four-wavefront one); lane l holds rows 4 (l / 16) .. 4 (l / 16) + 3 of column l % 16 of
+// each 16 x 16 tile.
 //
 // LDS layout (rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
 // c ^ ((r >> 1) & 7).  The LDS serves a 16-byte-per-lane read 16 lanes (256 B, 64 banks) at a
@@ -827,7 +818,7 @@ void lm_gemm_kernel(const GemmParams p) {
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = f32x16_t{};
   if constexpr (sizeof(T) == 2 && !Geo<T, MODE>::W8)
-    mainloop_bf16<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
+    mainloop_bf16_dw<MODE>(p, m0, n0, acc, smem);
   else if constexpr (sizeof(T) == 4)
     mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
 
@@ -1397,10 +1388,10 @@ static int launch_gemm(GemmParams p, int kind, double flops, hipStream_t stream)
   p.nnb = int((p.N + kBN - 1) / kBN);
   const int64_t nblk = int64_t(p.nmb) * p.nnb;
   if (nblk == 0) return FASTRL_OK;
-  FR_CHECK_ARG(sizeof(T) != 2 || MODE == MODE_FWD ||
+  FR_CHECK_ARG(sizeof(T) != 2 || MODE != MODE_DW ||
                    (p.K % 64 == 0 && p.lda < (int64_t(1) << 23) && p.ldb < (int64_t(1) << 23)),
                FASTRL_ERR_UNSUPPORTED,
-               "backward GEMM: K must be a multiple of 64 and leading dimensions below 2^23");
+               "dW GEMM: K must be a multiple of 64 and leading dimensions below 2^23");
   ProfScope prof(kind, stream, flops);
   hipLaunchKernelGGL((lm_gemm_kernel<T, MODE>), dim3(unsigned(nblk)), dim3(Geo<T, MODE>::THREADS), 0,
                      stream, p);
