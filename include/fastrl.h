@@ -247,7 +247,7 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
  *   training, Sec. 4), accumulated in the same pass as the log-sum-exp (one more partial
  *   sum exp(z - s_t) z per vocabulary block).  entropy_sum [1] float (may be NULL): sum_t H_t
  *   in float64, fixed order (the mean entropy is entropy_sum / T).
- * Limits: d % 8 == 0; hidden and W 16-byte aligned (FASTRL_ERR_VALUE); S >= 0; every
+ * Limits: d % 8 == 0; hidden, W and dW 16-byte aligned (FASTRL_ERR_VALUE); S >= 0; every
  *   sequence no longer than the slab (slab_tokens; 0 picks the largest slab whose exp-logit
  *   buffer stays within 48 GiB, ~169K tokens at V = 152064 in bf16; a longer sequence raises
  *   the slab to its length).  The tokens are spread over ceil(T / slab_tokens) slabs of about

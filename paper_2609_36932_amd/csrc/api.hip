@@ -238,6 +238,8 @@ static int check_loss_args(const fastrl_loss_args* a, bool need_ws) {
                  "fastrl_policy_loss: hidden / W / token_ids / old_logp is NULL");
     FR_CHECK_ARG(aligned16(a->hidden) && aligned16(a->W), FASTRL_ERR_VALUE,
                  "fastrl_policy_loss: hidden and W must be 16-byte aligned");
+    FR_CHECK_ARG(aligned16(a->dW), FASTRL_ERR_VALUE,
+                 "fastrl_policy_loss: dW must be 16-byte aligned");
   }
   FR_CHECK_ARG(a->S == 0 || a->adv, FASTRL_ERR_NULL_PTR, "fastrl_policy_loss: adv is NULL");
   FR_CHECK_ARG(a->beta == 0.0f || a->ref_logp || a->T == 0, FASTRL_ERR_NULL_PTR,

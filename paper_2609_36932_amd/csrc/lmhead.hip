@@ -5,12 +5,11 @@
 // of z = H W^T and g = dL/dlogp:  dZ = g (onehot(y) - P),  dH = dZ W,  dW = dZ^T H.
 //
 // One tiled GEMM kernel does the three contractions.  C[m, n] = sum_k A[m, k] B[n, k]
-// with both operands K-contiguous ("NT"), 256 x 256 block tiles, LDS double buffering, and
-// 32 x 32 MFMA tiles:
-//   bf16: 8 wavefronts of 128 x 64, v_mfma_f32_32x32x16_bf16, 64-wide K steps;
-//   f32:  4 wavefronts of 128 x 128, v_mfma_f32_32x32x2_f32.
-// Both engines leave the accumulators in the same register layout, so the epilogues are
-// shared.  Work is cut into slabs of whole sequences; per slab:
+// with 256 x 256 block tiles and LDS double buffering:
+//   bf16: 8 wavefronts of 128 x 64, v_mfma_f32_16x16x32_bf16, 64-wide K steps, operands moved
+//         by direct global->LDS loads;
+//   f32:  4 wavefronts of 128 x 128, v_mfma_f32_32x32x2_f32, register-staged loads.
+// Work is cut into slabs of whole sequences; per slab:
 //   FWD  C = W . H_slab^T  (rows = vocab, cols = tokens, K = d).  Epilogue: per token,
 //        the block's max and sum exp(z - s_t) over its 256 vocab rows (in-lane over 64
 //        values, then one lane swap and one LDS exchange), the sampled token's logit, and
@@ -20,8 +19,9 @@
 //   loss    g_t and c_t = g_t exp(s_t - lse_t) per token (one block per sequence).
 //   DH   C = E1 . W^T  (rows = tokens, cols = d, K = vocab):
 //        dH[t] = g_t W[y_t] - c_t C[t].
-//   DW   C = E1^T . Bd^T with Bd[n][t] = c_t H[t][n]  (rows = vocab, cols = d, K = tokens;
-//        E1 is read K-major through transposing LDS reads):
+//   DW   with Bd[n][t] = c_t H[t][n] (K = tokens; E1 is read K-major through transposing LDS
+//        reads): bf16 computes C' = Bd . E1 (rows = d, cols = vocab), f32 computes
+//        C = E1^T . Bd^T (rows = vocab, cols = d):
 //        dW[v] (+)= -C[v] + sum_{t in slab, y_t = v} g_t H[t].
 // Nothing of size [T, V] exists; the slab buffers hold [slab, V].
 #include <algorithm>
@@ -39,14 +39,17 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 256, kBN = 256;
 
-enum GemmMode { MODE_FWD = 0, MODE_DH = 1, MODE_DW = 2 };
+// MODE_DWT: the bf16 dW GEMM computed transposed, dW^T = Bd E (rows = hidden columns, cols =
+// vocab rows, K = tokens), so that it runs on the 8-wavefront engine with E as a K-major B
+enum GemmMode { MODE_FWD = 0, MODE_DH = 1, MODE_DW = 2, MODE_DWT = 3 };
 
-// wavefront geometry of the 256 x 256 block tile: the bf16 logits and dhidden GEMMs run 8
-// wavefronts (two per SIMD) of 128 x 64 on 16 x 16 x 32 MFMAs; the bf16 dW GEMM and every
-// float32 GEMM run 4 wavefronts of 128 x 128 on 32 x 32 MFMAs
+// wavefront geometry of the 256 x 256 block tile: every bf16 GEMM runs 8 wavefronts (two per
+// SIMD) of 128 x 64 on 16 x 16 x 32 MFMAs; every float32 GEMM runs 4 wavefronts of 128 x 128
+// on 32 x 32 MFMAs
 template <typename T, int MODE>
 struct Geo {
-  static constexpr bool W8 = sizeof(T) == 2 && MODE != MODE_DW;
+  static constexpr bool W8 = sizeof(T) == 2;
+  static_assert(MODE != (W8 ? MODE_DW : MODE_DWT), "dW runs transposed in bf16 only");
   static constexpr int THREADS = W8 ? 512 : 256, WAVES_N = W8 ? 4 : 2, NI = W8 ? 2 : 4,
                        WPE = W8 ? 2 : 1;
 };
@@ -119,14 +122,18 @@ constexpr int kGroupFwd = 32, kGroupDh = 4, kGroupDw = 4;
 template <int MODE>
 __device__ __forceinline__ void tile_coords(int& mb, int& nb, int nmb, int nnb) {
   const int b = blockIdx.x;
-  constexpr int GROUP = MODE == 0 ? kGroupFwd : MODE == 1 ? kGroupDh : kGroupDw;
-  const int per_group = GROUP * nnb;
+  constexpr int GROUP = MODE == MODE_FWD ? kGroupFwd : MODE == MODE_DH ? kGroupDh : kGroupDw;
+  // the groups are vocab blocks in both dW forms: M blocks of MODE_DW, N blocks of MODE_DWT
+  constexpr bool GN = MODE == MODE_DWT;
+  const int ng = GN ? nnb : nmb, ns = GN ? nmb : nnb;
+  const int per_group = GROUP * ns;
   const int gid = b / per_group;
   const int first = gid * GROUP;
-  const int gsz = min(nmb - first, GROUP);
+  const int gsz = min(ng - first, GROUP);
   const int in = b % per_group;
-  mb = first + in % gsz;
-  nb = in / gsz;
+  const int a = first + in % gsz, sweep = in / gsz;
+  mb = GN ? sweep : a;
+  nb = GN ? a : sweep;
 }
 
 template <typename T>
@@ -158,210 +165,11 @@ __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
   return wn * (kBN / Geo<T, MODE>::WAVES_N) + ni * 32 + (lane & 31);
 }
 
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
-
-// bf16 main loop of the dW GEMM (dW = E^T Bd^T: A = the slab's exp-logit tile E read K-major,
-// B = the scaled hidden rows Bd).  Four wavefronts (one per SIMD) each own a 128 x 128 part of
-// the block tile.
-// Operand tiles of 64 k move global -> registers -> LDS through two register sets and two LDS
-// stages (a 256 x 64 A tile and a 256 x 64 B tile, 64 KB per stage).  Iteration kt:
-//   k-steps 0-1  MFMAs of tile kt; loads of tile kt+2 into register set kt % 2
-//   k-step 2     MFMAs of tile kt; tile kt+1 (register set (kt+1) % 2, loaded during iteration
-//                kt-1) written to LDS stage (kt+1) % 2, which nobody reads since the last barrier
-//   k-step 3     half of the MFMAs, barrier, the first fragments of tile kt+1 read under the
-//                other half
-// A load thus has more than one iteration to land, and every wait on memory is the compiler's
-// own vmcnt / lgkmcnt wait for the registers an instruction reads.  Inside each k-step the 16
-// MFMAs are interleaved with the next k-step's 8 fragment reads and the step's loads or LDS
-// writes.
-//
-// B (K-contiguous, rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
-// c ^ ((r >> 1) & 7).  A fragment read (16 lanes = 16 rows of one chunk per LDS cycle) lands on
-// 16 distinct 16-byte bank groups, and a staging write covers whole rows (8 lanes per row).
-//
-// A (K-major: A[m][k] stored at k * lda + m, the exp tile E[t][v] read as E^T): the tile is 64
-// rows of k x 256 m (512 B), row k keeping its m-chunk c in slot c ^ ((k & 3) << 2).  Fragments come from ds_read_b64_tr_b16: inside each 16-lane group,
-// source lane j reads 4 consecutive m of row kbase + j/4 at m = mbase + 4 (j % 4), and lane i
-// receives A[mbase + i][kbase .. kbase + 3] -- 4 consecutive k of one row m, as the MFMA wants.
-constexpr int kTileP = kBM * 64;  // elements per operand per stage
-
-// K is a multiple of 64 (the padded slab), and the leading dimensions stay below 8M elements
-// (checked at launch).
-template <int MODE>
-__device__ __forceinline__ void mainloop_bf16_dw(const GemmParams& p, int m0, int n0,
-                                                 f32x16_t (&acc)[4][4], uint16_t* smem) {
-  static_assert(MODE == MODE_DW, "the logits and dhidden GEMMs run the 8-wavefront engine");
-  constexpr int BK = 64;
-  constexpr int TILE = kTileP;
-  constexpr int STAGE = 2 * TILE;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int K = p.K;
-  const int nk = (K + BK - 1) / BK;
-
-  // staging: load j (0..7) of B moves row 32 j + tid / 8, k-chunk tid % 8; of A, k row
-  // 8 j + tid / 32, m-chunk tid % 32.  Addresses are 32-bit byte offsets from a per-block base.
-  const int srow = tid >> 3, sch = tid & 7;
-  const int krow = tid >> 5, mch = tid & 31;
-  const char* Ab = reinterpret_cast<const char*>(static_cast<const uint16_t*>(p.A) + m0);
-  const char* Bb = reinterpret_cast<const char*>(static_cast<const uint16_t*>(p.B) +
-                                                 int64_t(n0) * p.ldb);
-  // byte offsets of this lane's 16-byte chunks from the tile base (below 2^32 for any
-  // leading dimension under 8M elements)
-  uint32_t ao[8], bo[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int r = 32 * j + srow;
-    ao[j] = (uint32_t(krow + 8 * j) * uint32_t(p.lda) + mch * 8) * 2;
-    // rows past the edge load a valid row; their results are never stored
-    bo[j] = (uint32_t(min(r, p.N - 1 - n0)) * uint32_t(p.ldb) + sch * 8) * 2;
-  }
-  const int64_t a_tile = int64_t(BK) * p.lda * 2;  // bytes per k-tile of A
-
-  // loads j = 4 h .. 4 h + 3 of tile kt
-  auto load_half = [&](int kt, int h, u32x4_t (&ra)[8], u32x4_t (&rb)[8]) {
-    const char* At = Ab + kt * a_tile;
-    const char* Bt = Bb + kt * (BK * 2);
-#pragma unroll
-    for (int j = 4 * h; j < 4 * h + 4; ++j) {
-      ra[j] = *reinterpret_cast<const u32x4_t*>(At + ao[j]);
-      rb[j] = *reinterpret_cast<const u32x4_t*>(Bt + bo[j]);
-    }
-  };
-  // LDS slots this lane writes (operand-relative; load j adds 32 j rows, or 8 j k-rows)
-  const int wk = srow * BK + (sch ^ ((srow >> 1) & 7)) * 8;
-  constexpr int WJ = 32 * BK;  // elements between staging rows j, j+1
-  const int wkm = krow * kBM + (mch ^ ((krow & 3) << 2)) * 8;
-  auto write_tile = [&](int stage, const u32x4_t (&ra)[8], const u32x4_t (&rb)[8]) {
-    uint16_t* sa = smem + stage * STAGE;
-    uint16_t* sb = sa + TILE;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      *reinterpret_cast<u32x4_t*>(sa + wkm + j * 8 * kBM) = ra[j];
-      *reinterpret_cast<u32x4_t*>(sb + wk + j * WJ) = rb[j];
-    }
-  };
-
-  // A fragment source: group g = lane / 16, i = lane % 16 reads row
-  // k = 8 (g / 2) + 4 s + i / 4 (s = first / second half of the 8 k), m = 16 (g % 2) + 4 (i % 4)
-  const int tg = lane >> 4, ti = lane & 15;
-  const int tr_k = 8 * (tg >> 1) + (ti >> 2);
-  const int tr_m = 16 * (tg & 1) + 4 * (ti & 3);
-  // issued in the order the MFMAs consume them: A row 0, the B columns, A rows 1-3
-  auto read_frags = [&](int stage, int kk, bf16x8_t (&fa)[4], bf16x8_t (&fb)[4]) {
-    const uint16_t* as = smem + stage * STAGE;
-    const uint16_t* bs = as + TILE;
-    // B: row (lane & 31) of a 32-row block, k-chunk 2 kk + lane / 32
-    const int fo = (lane & 31) * BK + ((kk * 2 + (lane >> 5)) ^ ((lane >> 1) & 7)) * 8;
-    auto read_a = [&](int i) {
-      const int m = wm * 128 + i * 32 + tr_m;
-      s16x4_t h[2];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int k = kk * 16 + tr_k + 4 * hh;
-        const int c = (m >> 3) ^ ((k & 3) << 2);
-        h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_s16x4_t*)(as + k * kBM + c * 8 + (m & 7)));
-      }
-      typedef short s16x8_t __attribute__((ext_vector_type(8)));
-      const s16x8_t v = {h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
-      fa[i] = __builtin_bit_cast(bf16x8_t, v);
-    };
-    read_a(0);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + fo + (wn * 128 + j * 32) * BK);
-#pragma unroll
-    for (int i = 1; i < 4; ++i) read_a(i);
-  };
-  auto mma_rows = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4], int i0, int i1) {
-#pragma unroll
-    for (int i = i0; i < i1; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-  };
-  // fragment reads of one k-step: 8 transposing A reads and 4 B reads
-  constexpr int NFR = 12;
-  constexpr int NFR_SLOT = (NFR + 7) / 8;  // reads per interleave slot (8 slots per k-step)
-
-  // one k-step's order: the next k-step's fragment reads and `n` instructions of class `mask`
-  // (global loads or LDS writes) alternate between the 16 MFMAs
-#define ORDER_READS_THEN(mask, n)                                     \
-  do {                                                                \
-    _Pragma("unroll") for (int q_ = 0; q_ < 8; ++q_) {                \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              \
-      __builtin_amdgcn_sched_group_barrier(0x100, NFR_SLOT, 0);       \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              \
-      __builtin_amdgcn_sched_group_barrier(mask, n, 0);               \
-    }                                                                 \
-  } while (0)
-  bf16x8_t fa0[4], fb0[4], fa1[4], fb1[4];
-  u32x4_t ra0[8], rb0[8], ra1[8], rb1[8];
-  auto iteration = [&](auto stage, int kt, u32x4_t (&la)[8], u32x4_t (&lb)[8], u32x4_t (&wa)[8],
-                       u32x4_t (&wb)[8]) {
-    constexpr int cur = decltype(stage)::value;
-    // the last iterations re-load and re-write the last tile into the unused stage (never
-    // read): keeps every iteration branch-free so its loads interleave with the MFMAs
-    const int tl = min(kt + 2, nk - 1);
-    // ---- k-step 0: loads of tile kt+2, first half
-    read_frags(cur, 1, fa1, fb1);
-    load_half(tl, 0, la, lb);
-    mma_rows(fa0, fb0, 0, 4);
-    ORDER_READS_THEN(0x020, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    // ---- k-step 1: second half
-    read_frags(cur, 2, fa0, fb0);
-    load_half(tl, 1, la, lb);
-    mma_rows(fa1, fb1, 0, 4);
-    ORDER_READS_THEN(0x020, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    // ---- k-step 2: tile kt+1 to the other stage
-    read_frags(cur, 3, fa1, fb1);
-    write_tile(cur ^ 1, wa, wb);
-    mma_rows(fa0, fb0, 0, 4);
-    ORDER_READS_THEN(0x200, 2);
-    __builtin_amdgcn_sched_barrier(0);
-    // ---- k-step 3: half the MFMAs cover the write completion and the barrier, the other
-    // half the first fragment reads of tile kt+1
-    mma_rows(fa1, fb1, 0, 2);
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    __builtin_amdgcn_sched_barrier(0);
-    read_frags(cur ^ 1, 0, fa0, fb0);
-    mma_rows(fa1, fb1, 2, 4);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, NFR_SLOT, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
-  // prologue: tile 0 in stage 0, tile 1 in flight in register set 1
-  load_half(0, 0, ra0, rb0);
-  load_half(0, 1, ra0, rb0);
-  load_half(min(1, nk - 1), 0, ra1, rb1);
-  load_half(min(1, nk - 1), 1, ra1, rb1);
-  write_tile(0, ra0, rb0);
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  read_frags(0, 0, fa0, fb0);
-  int kt = 0;
-  for (; kt + 1 < nk; kt += 2) {
-    iteration(std::integral_constant<int, 0>{}, kt, ra0, rb0, ra1, rb1);
-    iteration(std::integral_constant<int, 1>{}, kt + 1, ra1, rb1, ra0, rb0);
-  }
-  if (kt < nk) iteration(std::integral_constant<int, 0>{}, kt, ra0, rb0, ra1, rb1);
-#undef ORDER_READS_THEN
-}
-
-
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// bf16 main loop of the logits GEMM (z = W h: A = LM-head rows, B = gathered hidden rows, K = d)
-// and of the dhidden GEMM (A = the slab's exp-logit rows, B = W^T rows, K = padded vocab).
+// bf16 main loop of the logits GEMM (z = W h: A = LM-head rows, B = gathered hidden rows, K = d),
+// the dhidden GEMM (A = the slab's exp-logit rows, B = W^T rows, K = padded vocab) and the
+// transposed dW GEMM (A = Bd rows, B = the exp-logit tile read K-major, K = padded slab).
 // Eight wavefronts (two per SIMD, so one can issue MFMAs while the other waits on memory) each
 // own a 128 x 64 part of the block tile.  LDS holds two stages of a 256 x 64 A tile and a
 // 256 x 64 B tile (32 KB each), written by direct global->LDS loads (global_load_lds_dwordx4):
@@ -370,9 +178,9 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // fragments of k-step kk+1 are read while the MFMAs of k-step kk run.  The MFMAs are
 // v_mfma_f32_16x16x32_bf16 (8 x 4 tiles of 16 x 16 per wavefront, two 32-k steps per tile):
 // per FLOP they move less accumulator data through the register file than 32 x 32 x 16, and
-// measured 7% faster on the logits GEMM and 4% on dhidden (where this engine also beat the
-// four-wavefront one); lane l holds rows 4 (l / 16) .. 4 (l / 16) + 3 of column l % 16 of
-// each 16 x 16 tile.
+// measured 7% faster on the logits GEMM and 4% on dhidden (where this engine also beat a
+// four-wavefront one, as it does on dW); lane l holds rows 4 (l / 16) .. 4 (l / 16) + 3 of
+// column l % 16 of each 16 x 16 tile.
 //
 // LDS layout (rows of 64 k = 128 B): row r keeps its k-chunk c (8 bf16) in slot
 // c ^ ((r >> 1) & 7).  The LDS serves a 16-byte-per-lane read 16 lanes (256 B, 64 banks) at a
@@ -383,6 +191,7 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
                                                   f32x4_t (&acc)[8][4], uint16_t* smem) {
   constexpr int BK = 64;
   constexpr int TILE = kBM * BK;  // elements per operand per stage
+  constexpr bool BKM = MODE == MODE_DWT;  // B stored K-major (B[n][k] at k * ldb + n)
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
@@ -398,10 +207,52 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     const int r = wave * 32 + j * 8 + lrow;
     const int ra = min(m0 + r, p.M - 1);  // rows past the edge load a valid row; their
     arow[j] = int64_t(ra) * p.lda;        // results are never stored
-    int64_t br = min(n0 + r, p.N - 1) + p.b_row_base;
-    if (p.b_rows) br = p.b_rows[br];
-    brow[j] = br * p.ldb;
+    if constexpr (BKM) {
+      // K-major B tile: 64 k-rows of 256 n (512 B); load j of this wavefront fills k-rows
+      // 8 wave + 2 j and the next, lane l slot l % 32 of row 8 wave + 2 j + l / 32, with the
+      // n-chunk that belongs there (slot = chunk ^ kmaj_swz(k))
+      const int k = wave * 8 + 2 * j + (lane >> 5);
+      const int swz = ((k & 3) << 1) | (((k >> 3) & 1) << 3);
+      brow[j] = int64_t(k) * p.ldb + n0 + (((lane & 31) ^ swz) << 3);
+    } else {
+      int64_t br = min(n0 + r, p.N - 1) + p.b_row_base;
+      if (p.b_rows) br = p.b_rows[br];
+      brow[j] = br * p.ldb;
+    }
   }
+  // K-major B fragments (ds_read_b64_tr_b16): in 16-lane group g, lane jj reads 4 n of k-row
+  // 8 g + 4 s + jj / 4 (s = first / second 4 k of the lane's 8) at n = 16 j + 4 (jj % 4) of
+  // the wavefront's 64 columns, and receives the 4 k of column n = 16 j + jj.  The row swizzle
+  // puts the 8 rows that lanes 0-31 (and 32-63) read on 16 distinct 16-byte bank groups.
+  int bfo[4];
+  if constexpr (BKM) {
+    const int g = lane >> 4, jj = lane & 15;
+    const int swz = ((jj >> 2) << 1) | ((g & 1) << 3);  // kmaj_swz of the rows this lane reads
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = wn * 64 + 16 * j + 4 * (jj & 3);
+      bfo[j] = (8 * g + (jj >> 2)) * kBN + (((n >> 3) ^ swz) << 3) + (n & 7);
+    }
+  }
+  // The transposing reads are issued as inline assembly: before the builtin form the compiler
+  // waits for every outstanding direct-to-LDS load (it cannot tell the two stages apart), which
+  // drains the next tile's prefetch in every k-step (measured 10% slower).  Their results are
+  // waited for explicitly (frag_wait) before the MFMAs that read them, and before the barrier
+  // that hands their stage back to the loads.
+  uint32_t bfa[4];  // LDS byte addresses of this lane's K-major B fragments in stage 0
+  if constexpr (BKM) {
+    typedef __attribute__((address_space(3))) const uint16_t lds_u16_t;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      bfa[j] = uint32_t(uintptr_t((lds_u16_t*)(smem + TILE + bfo[j])));
+  }
+  auto frag_wait = [&]() {
+    if constexpr (BKM) {
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
   const int K = p.K;
   const int nk = (K + BK - 1) / BK;
   const bool ktail = (K % BK) != 0;
@@ -415,7 +266,9 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     for (int j = 0; j < 4; ++j) {
       const int kc = (j & 1) ? kc1 : kc0;
       __builtin_amdgcn_global_load_lds(Ag + arow[j] + kc, (lds_void_t*)(sa + j * 8 * BK), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(Bg + brow[j] + kc, (lds_void_t*)(sb + j * 8 * BK), 16, 0, 0);
+      // (K-major B: k-rows 8 wave + 2 j, + 1 start at the same LDS offset as rows 32 wave + 8 j)
+      const uint16_t* bsrc = BKM ? Bg + brow[j] + int64_t(kt) * BK * p.ldb : Bg + brow[j] + kc;
+      __builtin_amdgcn_global_load_lds(bsrc, (lds_void_t*)(sb + j * 8 * BK), 16, 0, 0);
     }
   };
   auto zero_tail = [&](int kt, int stage) {  // this lane's slots past K in tile kt
@@ -435,12 +288,37 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     const uint16_t* as = smem + stage * 2 * TILE;
     const uint16_t* bs = as + TILE;
     const int slot = ((kk * 4 + (lane >> 4)) ^ sw) * 8;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
+    auto read_a = [&](int i) {
       fa[i] = *reinterpret_cast<const bf16x8_t*>(as + (wm * 128 + i * 16 + (lane & 15)) * BK + slot);
+    };
+    if constexpr (BKM) {
+      // program order A0 B0 A1 B1 .. A3 B3 A4 .. A7: the reads stay in this order, so pinning
+      // the A reads among the MFMAs spreads the B reads too
+      const uint32_t sofs = uint32_t(stage) * (2 * TILE * 2);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 64 + j * 16 + (lane & 15)) * BK + slot);
+      for (int j = 0; j < 4; ++j) {
+        read_a(j);
+        typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+        u32x2_t h0, h1;
+        const uint32_t a = bfa[j] + sofs;
+        if (kk == 0) {
+          asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(h0) : "v"(a) : "memory");
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:2048" : "=v"(h1) : "v"(a) : "memory");
+        } else {
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:16384" : "=v"(h0) : "v"(a) : "memory");
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:18432" : "=v"(h1) : "v"(a) : "memory");
+        }
+        fb[j] = __builtin_bit_cast(bf16x8_t, u32x4_t{h0[0], h0[1], h1[0], h1[1]});
+      }
+#pragma unroll
+      for (int i = 4; i < 8; ++i) read_a(i);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) read_a(i);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        fb[j] = *reinterpret_cast<const bf16x8_t*>(bs + (wn * 64 + j * 16 + (lane & 15)) * BK + slot);
+    }
   };
   auto mma = [&](const bf16x8_t (&fa)[8], const bf16x8_t (&fb)[4]) {
 #pragma unroll
@@ -458,17 +336,29 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
   };
 
   bf16x8_t fa0[8], fb0[4], fa1[8], fb1[4];
-  // pin the order inside a k-step: the 32 MFMAs of this step with the 12 fragment reads of the
+  // fragment reads per k-step that the scheduler places: 8 A reads and 4 B reads, or (K-major
+  // B) the 8 A reads, each followed in program order by the assembly B reads
+  constexpr int NRD = BKM ? 8 : 12;
+  // pin the order inside a k-step: the 32 MFMAs of this step with the fragment reads of the
   // next step spread among the first 24 (at most one step's reads in flight, so the wait before
   // the next step's MFMAs is exact, and the last read still has 8 MFMAs to land)
   auto kstep = [&](int stage, int kk_next, bf16x8_t (&fa)[8], bf16x8_t (&fb)[4],
                    bf16x8_t (&na)[8], bf16x8_t (&nb)[4]) {
+    frag_wait();
     frags(stage, kk_next, na, nb);
     mma(fa, fb);
+    if constexpr (BKM) {
 #pragma unroll
-    for (int q = 0; q < 12; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      for (int q = 0; q < 8; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 12; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     __builtin_amdgcn_sched_barrier(0);
@@ -485,6 +375,7 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     kstep(cur, 1, fa0, fb0, fa1, fb1);
     // last k-step: half of its MFMAs cover the barrier; the other half cover the next
     // tile's load issue and the first fragment reads of tile kt+1
+    frag_wait();
     mma_half(fa1, fb1, 0);
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tile kt+1 is in LDS
@@ -500,15 +391,16 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NRD / 2, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NRD / 2, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the re-load above has landed
   {  // last tile
     const int cur = kt & 1;
     kstep(cur, 1, fa0, fb0, fa1, fb1);
+    frag_wait();
     mma(fa1, fb1);
   }
 }
@@ -780,10 +672,41 @@ __device__ __forceinline__ void dh_epilogue_bf16(const GemmParams& p, int m0, in
     }
 }
 
+// Epilogue of the bf16 dW GEMM computed transposed (C' = Bd E on the 16 x 16 layout: acc[i][j]
+// holds hidden columns n = wm*128 + 16 i + 4 (l / 16) + q of vocab row v = wn*64 + 16 j + l % 16):
+// each lane owns 4 consecutive n of one dW row and moves them as one 16-byte access.
+// dW[v][n] (+)= -C'[n][v]; the one-hot part is added by dw_onehot_kernel.  Needs d % 4 == 0 and
+// a 16-byte aligned dW (checked on the host).
+__device__ __forceinline__ void dwt_epilogue_bf16(const GemmParams& p, int m0, int n0,
+                                                  f32x4_t (&acc)[8][4]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int nq = m0 + wm * 128 + 4 * (lane >> 4);  // first hidden column of acc[0][j]
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int v = n0 + wn * 64 + 16 * j + (lane & 15);
+    if (v < p.N) {
+      f32x4_t* row = reinterpret_cast<f32x4_t*>(p.dW + int64_t(v) * p.d);
+      // every load of the row first, so that their latencies overlap
+      f32x4_t prev[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int n = nq + 16 * i;
+        prev[i] = (p.dW_acc && n < p.M) ? row[n >> 2] : f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int n = nq + 16 * i;
+        if (n < p.M) row[n >> 2] = prev[i] - acc[i][j];
+      }
+    }
+  }
+}
+
 template <typename T>
 struct SmemBytes;
 template <>
-struct SmemBytes<uint16_t> { static constexpr int value = 2 * 2 * kTileP * 2; };
+struct SmemBytes<uint16_t> { static constexpr int value = 2 * 2 * kBM * 64 * 2; };
 template <>
 struct SmemBytes<float> { static constexpr int value = 2 * 2 * kBM * Eng<float>::LD * 4; };
 
@@ -809,7 +732,8 @@ void lm_gemm_kernel(const GemmParams p) {
       for (int j = 0; j < 4; ++j) acc16[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
     mainloop_bf16_dma<MODE>(p, m0, n0, acc16, smem);
     if constexpr (MODE == MODE_FWD) fwd_epilogue_bf16(p, m0, n0, mb, acc16, smem);
-    else dh_epilogue_bf16(p, m0, n0, acc16);
+    else if constexpr (MODE == MODE_DH) dh_epilogue_bf16(p, m0, n0, acc16);
+    else dwt_epilogue_bf16(p, m0, n0, acc16);
     return;
   }
   f32x16_t acc[4][NI];
@@ -817,10 +741,7 @@ void lm_gemm_kernel(const GemmParams p) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = f32x16_t{};
-  if constexpr (sizeof(T) == 2 && !Geo<T, MODE>::W8)
-    mainloop_bf16_dw<MODE>(p, m0, n0, acc, smem);
-  else if constexpr (sizeof(T) == 4)
-    mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
+  if constexpr (sizeof(T) == 4) mainloop_f32<MODE, MODE == MODE_DW>(p, m0, n0, acc, smem);
 
   // ------------------------------------------------------------------ epilogues
   if constexpr (MODE == MODE_FWD && sizeof(T) == 4) {  // float32 logits (bf16: fwd_epilogue_bf16)
@@ -961,8 +882,8 @@ void lm_gemm_kernel(const GemmParams p) {
         }
       }
   } else {  // MODE_DW: dW[v] (+)= -C[v]; the one-hot part is added by dw_onehot_kernel
-    // RB rows at a time (fewer where the float32 engine leaves fewer free registers)
-    constexpr int RB = sizeof(T) == 2 ? 8 : 4;
+    // RB rows at a time
+    constexpr int RB = 4;
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
@@ -1392,6 +1313,10 @@ static int launch_gemm(GemmParams p, int kind, double flops, hipStream_t stream)
                    (p.K % 64 == 0 && p.lda < (int64_t(1) << 23) && p.ldb < (int64_t(1) << 23)),
                FASTRL_ERR_UNSUPPORTED,
                "dW GEMM: K must be a multiple of 64 and leading dimensions below 2^23");
+  // transposed dW: whole 64-k tiles, whole 256-column tiles of the K-major E, 16-byte dW rows
+  FR_CHECK_ARG(MODE != MODE_DWT || (p.K % 64 == 0 && p.ldb >= int64_t(p.nnb) * kBN &&
+                                    p.ldb % 8 == 0 && p.d % 4 == 0 && p.M == p.d),
+               FASTRL_ERR_UNSUPPORTED, "transposed dW GEMM: unsupported shape");
   ProfScope prof(kind, stream, flops);
   hipLaunchKernelGGL((lm_gemm_kernel<T, MODE>), dim3(unsigned(nblk)), dim3(Geo<T, MODE>::THREADS), 0,
                      stream, p);
@@ -1678,13 +1603,19 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
                          w.lab_off, V, w.lab_tok);
       FR_LAUNCHED();
       GemmParams q{};
-      q.A = w.E1; q.lda = Vpad; q.M = V;  // read K-major: A[v][t] = E1[t][v]
-      q.B = w.Bd; q.ldb = tcp; q.N = d;
       q.K = int32_t(Tr);
       q.dW = a.dW; q.dW_acc = (si > 0 || a.dW_accumulate) ? 1 : 0;
       q.d = d;
       q.status = a.status;
-      FR_TRY((launch_gemm<T, MODE_DW>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
+      if constexpr (sizeof(T) == 2) {  // dW^T = Bd E: A = Bd, B = E1 read K-major
+        q.A = w.Bd; q.lda = tcp; q.M = d;
+        q.B = w.E1; q.ldb = Vpad; q.N = V;
+        FR_TRY((launch_gemm<T, MODE_DWT>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
+      } else {  // dW = E^T Bd^T: A = E1 read K-major (A[v][t] = E1[t][v]), B = Bd
+        q.A = w.E1; q.lda = Vpad; q.M = V;
+        q.B = w.Bd; q.ldb = tcp; q.N = d;
+        FR_TRY((launch_gemm<T, MODE_DW>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
+      }
       if (Tc > 0) {
         hipLaunchKernelGGL((dw_onehot_kernel<T>), dim3(unsigned(Tc)), dim3(256), 0, stream,
                            w.lab_off, w.lab_tok, w.yslab, w.gslab, static_cast<const T*>(a.hidden),

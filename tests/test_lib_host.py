@@ -113,7 +113,8 @@ def test_host_validation_errors(fr):
 
 
 def test_lm_head_operands_must_be_16_byte_aligned(fr):
-    """hidden and W are read in 16-byte pieces: a misaligned pointer is refused on the host."""
+    """hidden, W and dW are accessed in 16-byte pieces: a misaligned pointer is refused on
+    the host."""
     L = fr._lib
     p, q = ctypes.c_void_p(256), ctypes.c_void_p(258)
     assert L.fastrl_token_logprob(q, None, p, 1, 4, 16, 10, p, p, None, None, None, 0,
@@ -129,6 +130,10 @@ def test_lm_head_operands_must_be_16_byte_aligned(fr):
     a.hidden, a.W = p, q
     assert L.fastrl_policy_loss_fwd_bwd(ctypes.byref(a), None) == -3
     assert b"16-byte" in L.fastrl_last_error()
+    # dW is updated in 16-byte pieces too
+    a.W, a.dW = p, ctypes.c_void_p(264)
+    assert L.fastrl_policy_loss_fwd_bwd(ctypes.byref(a), None) == -3
+    assert b"dW must be 16-byte" in L.fastrl_last_error()
 
 
 def test_workspace_queries(fr):
