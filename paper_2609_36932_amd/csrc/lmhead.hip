@@ -246,10 +246,14 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     for (int j = 0; j < 4; ++j)
       bfa[j] = uint32_t(uintptr_t((lds_u16_t*)(smem + TILE + bfo[j])));
   }
-  auto frag_wait = [&]() {
+  // the B fragments pass through the wait as operands, so no use of them can precede it
+  auto frag_wait = [&](bf16x8_t (&fb)[4]) {
     if constexpr (BKM) {
       __builtin_amdgcn_sched_barrier(0);
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(fb[0]), "+v"(fb[1]), "+v"(fb[2]), "+v"(fb[3])
+                   :
+                   : "memory");
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -344,7 +348,7 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
   // the next step's MFMAs is exact, and the last read still has 8 MFMAs to land)
   auto kstep = [&](int stage, int kk_next, bf16x8_t (&fa)[8], bf16x8_t (&fb)[4],
                    bf16x8_t (&na)[8], bf16x8_t (&nb)[4]) {
-    frag_wait();
+    frag_wait(fb);
     frags(stage, kk_next, na, nb);
     mma(fa, fb);
     if constexpr (BKM) {
@@ -375,7 +379,7 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     kstep(cur, 1, fa0, fb0, fa1, fb1);
     // last k-step: half of its MFMAs cover the barrier; the other half cover the next
     // tile's load issue and the first fragment reads of tile kt+1
-    frag_wait();
+    frag_wait(fb1);
     mma_half(fa1, fb1, 0);
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tile kt+1 is in LDS
@@ -400,7 +404,7 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
   {  // last tile
     const int cur = kt & 1;
     kstep(cur, 1, fa0, fb0, fa1, fb1);
-    frag_wait();
+    frag_wait(fb1);
     mma(fa1, fb1);
   }
 }
