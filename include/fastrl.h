@@ -73,6 +73,8 @@ typedef enum fastrl_status {
 #define FASTRL_SB_BAD_GRAD      0x80  /* a non-finite gradient entry reached the optimizer */
 #define FASTRL_SB_FILL_SHORT    0x100 /* DP alignment: too few unselected trajectories to reach
                                          a multiple of dp_align */
+#define FASTRL_SB_SYNC_TIMEOUT  0x200 /* a GEMM block's wavefronts did not meet within the bounded
+                                         wait of its stage hand-over (results not reliable) */
 
 typedef enum fastrl_dtype { FASTRL_F32 = 0, FASTRL_BF16 = 1 } fastrl_dtype;
 typedef enum fastrl_algo { FASTRL_GRPO = 0, FASTRL_DAPO = 1, FASTRL_GSPO = 2 } fastrl_algo;

@@ -30,7 +30,7 @@ NORMS = {"seq_mean_token_mean": NORM_SEQ_MEAN_TOKEN_MEAN, "token_mean": NORM_TOK
 K_LOGITS_FWD, K_DHIDDEN, K_DW = 0, 1, 2
 STATUS_BITS = {0x1: "BAD_OFFSETS", 0x2: "BAD_TOKEN", 0x4: "GROUP_TOO_BIG",
                0x8: "SEQ_TOO_LONG", 0x10: "BAD_REWARD", 0x20: "BAD_INDEX",
-               0x40: "SHIFT_REDO", 0x80: "BAD_GRAD", 0x100: "FILL_SHORT"}
+               0x40: "SHIFT_REDO", 0x80: "BAD_GRAD", 0x100: "FILL_SHORT", 0x200: "SYNC_TIMEOUT"}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
