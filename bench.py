@@ -38,8 +38,8 @@ PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 MFMA
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--slab", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true")
@@ -114,11 +114,22 @@ def cpu_baseline(cfg, ro, inp, n_tokens):
     the whole batch, then the LM-head forward, loss and full backward (dH and dW at full
     V x d) for the first kept sequences holding >= n_tokens tokens."""
     import oracle
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        info = threadpool_info()
+        cores = max([i.get("num_threads", 1) for i in info] + [1])
+        blas = ",".join(sorted({i.get("internal_api", "?") for i in info if i.get("user_api") == "blas"})) or blas
     except Exception:
         cores = os.cpu_count()
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     H = inp["H"]
     Wd = inp["W"].float().cpu().numpy().astype(np.float64)
     old = inp["old"].cpu().numpy()
@@ -142,6 +153,7 @@ def cpu_baseline(cfg, ro, inp, n_tokens):
     dH, dW = oracle.lmhead_backward(Hk, Wd, y, lse, g)
     dt = time.perf_counter() - t0
     return dict(value=len(src) / dt, unit="kept tokens/s", cores=int(cores), kind="oracle",
+                cpu=cpu, blas=blas,
                 sample=f"whole batch advantage+MDAP+compaction, then LM-head fwd + loss + "
                        f"full bwd (dH, dW at V={cfg.V}, d={cfg.d}) in fp64 for the first "
                        f"{S} kept sequences ({len(src)} tokens); {dt:.1f} s")
