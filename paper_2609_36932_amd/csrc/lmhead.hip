@@ -11,8 +11,8 @@
 //   f32:  4 wavefronts of 128 x 128, v_mfma_f32_32x32x2_f32, register-staged loads.
 // Work is cut into slabs of whole sequences; per slab:
 //   FWD  C = W . H_slab^T  (rows = vocab, cols = tokens, K = d).  Epilogue: per token,
-//        the block's max and sum exp(z - s_t) over its 256 vocab rows (in-lane over 64
-//        values, then one lane swap and one LDS exchange), the sampled token's logit, and
+//        the block's max and sum exp(z - s_t) over its 256 vocab rows (in-lane over 32
+//        values, two lane shuffles, one LDS exchange), the sampled token's logit, and
 //        E1[t][v] = exp(z - s_t) (s_t = 0 unless exp(z) would leave float range).
 //   merge   partials -> lse, logp, row max; rows whose max is too far from s_t get
 //           s_t = max_t and their token block is evaluated again (rare), then merge again.
@@ -355,6 +355,10 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
   auto kstep = [&](int stage, int kk_next, bf16x8_t (&fa)[8], bf16x8_t (&fb)[4],
                    bf16x8_t (&na)[8], bf16x8_t (&nb)[4]) {
     frag_wait(fb);
+    // raised wave priority while this k-step's MFMAs issue: the SIMD's other wavefront (at a
+    // barrier, its loads or its epilogue) yields the issue slots (+1-4% on dW, +0-2% on
+    // dhidden; the hand-over block and a higher level measured no better)
+    __builtin_amdgcn_s_setprio(1);
     frags(stage, kk_next, na, nb);
     mma(fa, fb);
     if constexpr (BKM) {
@@ -372,6 +376,7 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(0);
   };
   // Long-K GEMMs (dhidden, dW) hand a stage over with a split barrier on an LDS counter: a
   // wavefront arrives (adds 1) once its own loads of tile kt+1 have landed and its own reads of
