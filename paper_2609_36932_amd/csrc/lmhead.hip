@@ -217,11 +217,23 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
       const int k = wave * 8 + 2 * j + (lane >> 5);
       const int swz = ((k & 3) << 1) | (((k >> 3) & 1) << 3);
       brow[j] = int64_t(k) * p.ldb + n0 + (((lane & 31) ^ swz) << 3);
-    } else {
-      int64_t br = min(n0 + r, p.N - 1) + p.b_row_base;
-      if (p.b_rows) br = p.b_rows[br];
-      brow[j] = br * p.ldb;
     }
+  }
+  if constexpr (!BKM) {
+    // B rows, gathered through b_rows when given: the four index loads are issued together
+    // (one memory round trip before the first tile load, not four one after the other)
+    int64_t bi[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bi[j] = min(n0 + wave * 32 + j * 8 + lrow, p.N - 1) + p.b_row_base;
+    if (p.b_rows) {
+      int32_t g[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) g[j] = __builtin_nontemporal_load(p.b_rows + bi[j]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bi[j] = g[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) brow[j] = bi[j] * p.ldb;
   }
   // K-major B fragments (ds_read_b64_tr_b16): in 16-lane group g, lane jj reads 4 n of k-row
   // 8 g + 4 s + jj / 4 (s = first / second 4 k of the lane's 8) at n = 16 j + 4 (jj % 4) of
