@@ -217,3 +217,12 @@ def test_binding_rejects_host_tensors(fr):
         fr._arg(torch.zeros(4, dtype=torch.int32), torch.int32, "x")
     with pytest.raises(fr.FastRLError, match="device tensor"):
         fr.advantage(torch.zeros(4), torch.tensor([0, 4], dtype=torch.int32))
+
+
+def test_status_bits_match_header(fr):
+    """The binding names every device status bit the header defines, with the same value."""
+    src = open(HEADER).read()
+    bits = {int(v, 16): n for n, v in re.findall(r"#define FASTRL_SB_(\w+)\s+(0x[0-9a-fA-F]+)", src)}
+    assert len(bits) >= 10
+    assert bits == fr.STATUS_BITS
+    assert fr.status_names(0x200) == ["SYNC_TIMEOUT"]
