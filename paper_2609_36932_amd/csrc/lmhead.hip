@@ -408,8 +408,10 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
   __syncthreads();
   frags(0, 0, fa0, fb0);
   if (nk > 1) issue(1, 1);
-  int kt = 0;
-  for (; kt + 1 < nk; ++kt) {
+  // one 64-wide tile with its hand-over; LOAD: tile kt+2 exists and is loaded into the stage
+  // tile kt frees (false only for the last hand-over)
+  auto iteration = [&](int kt, auto load) {
+    constexpr bool LOAD = decltype(load)::value;
     const int cur = kt & 1;
     kstep(cur, 1, fa0, fb0, fa1, fb1);
     // last k-step: half of its MFMAs cover the barrier; the other half cover the next
@@ -445,22 +447,24 @@ __device__ __forceinline__ void mainloop_bf16_dma(const GemmParams& p, int m0, i
       if (kt + 2 == nk && ktail) zero_tail(kt + 1, cur ^ 1);
       __syncthreads();                                   // and nobody reads tile kt any more
     }
-    // the last two iterations re-load tile nk-1 into the free stage (never read): keeps
-    // this block branch-free so the loads can interleave with the MFMAs
-    issue(min(kt + 2, nk - 1), cur);
+    if constexpr (LOAD) issue(kt + 2, cur);
     frags(cur ^ 1, 0, fa0, fb0);
     mma_half(fa1, fb1, 1);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    if constexpr (LOAD) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    }
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, NRD / 2, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, NRD / 2, 0);
     __builtin_amdgcn_sched_barrier(0);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the re-load above has landed
+  };
+  int kt = 0;
+  for (; kt + 2 < nk; ++kt) iteration(kt, std::true_type{});
+  if (kt + 1 < nk) iteration(kt++, std::false_type{});
   {  // last tile
     const int cur = kt & 1;
     kstep(cur, 1, fa0, fb0, fa1, fb1);
