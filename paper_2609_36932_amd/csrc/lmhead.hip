@@ -623,48 +623,63 @@ __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, i
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     if (g == 0) xmax[wm * kBN + cl] = mx;
     if (rel) {
-      float ssp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, zsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
       uint16_t* e1 = static_cast<uint16_t*>(p.E1) + int64_t(t) * p.ldE1;
+      // exp(z - s_t) = exp2(z log2e - s_t log2e): one FMA and v_exp_f32 per logit (s_t = +inf
+      // past the slab gives 0).  Two uniform choices get code of their own, since this pass is
+      // most of the epilogue (a per-block timing probe: 8.5% of the kernel): the row check only
+      // in the last vocab block, the z-weighted sum only when the entropy is asked for.
+      const float sl = s_t * 1.4426950408889634f;
+      auto pass = [&](auto full_c, auto z_c) {
+        constexpr bool FULL = decltype(full_c)::value, WZ = decltype(z_c)::value;
+        float ssp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, zsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int ip = 0; ip < 4; ++ip) {  // tile pair 2 ip, 2 ip + 1
-        uint32_t pk[2][2];
+        for (int ip = 0; ip < 4; ++ip) {  // tile pair 2 ip, 2 ip + 1
+          uint32_t pk[2][2];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int i = 2 * ip + h;
-          float e[4];
+          for (int h = 0; h < 2; ++h) {
+            const int i = 2 * ip + h;
+            float e[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            e[q] = __expf(acc[i][j][q] - s_t);
-            if (!rows_full && rbase + 16 * i + q >= Vr) e[q] = 0.0f;
-            ssp[ip] += e[q];
-            zsp[ip] = fmaf(e[q], acc[i][j][q], zsp[ip]);
+            for (int q = 0; q < 4; ++q) {
+              e[q] = __builtin_amdgcn_exp2f(fmaf(acc[i][j][q], 1.4426950408889634f, -sl));
+              if (!FULL && rbase + 16 * i + q >= Vr) e[q] = 0.0f;
+              ssp[ip] += e[q];
+              if (WZ) zsp[ip] = fmaf(e[q], acc[i][j][q], zsp[ip]);
+            }
+            typedef float f32x2_t __attribute__((ext_vector_type(2)));
+            typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+            pk[h][0] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[0], e[1]}, bf16x2_t));
+            pk[h][1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[2], e[3]}, bf16x2_t));
           }
-          typedef float f32x2_t __attribute__((ext_vector_type(2)));
-          typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-          pk[h][0] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[0], e[1]}, bf16x2_t));
-          pk[h][1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{e[2], e[3]}, bf16x2_t));
-        }
-        // lane group g holds rows 4 g .. 4 g + 3 of both tiles; one swap between the groups of
-        // each 32-lane half (odd group's tile-2ip rows <-> even group's tile-2ip+1 rows) leaves
-        // group g with 8 consecutive rows: tile 2 ip + (g & 1), rows 8 (g >> 1) .. + 7
+          // lane group g holds rows 4 g .. 4 g + 3 of both tiles; one swap between the groups
+          // of each 32-lane half (odd group's tile-2ip rows <-> even group's tile-2ip+1 rows)
+          // leaves group g with 8 consecutive rows: tile 2 ip + (g & 1), rows 8 (g >> 1) .. + 7
 #pragma unroll
-        for (int w = 0; w < 2; ++w) {
-          const auto sw = __builtin_amdgcn_permlane16_swap(pk[0][w], pk[1][w], false, false);
-          pk[0][w] = sw[0];
-          pk[1][w] = sw[1];
+          for (int w = 0; w < 2; ++w) {
+            const auto sw = __builtin_amdgcn_permlane16_swap(pk[0][w], pk[1][w], false, false);
+            pk[0][w] = sw[0];
+            pk[1][w] = sw[1];
+          }
+          const int v0 = m0 + wm * 128 + (2 * ip + (g & 1)) * 16 + (g >> 1) * 8;
+          *reinterpret_cast<uint4*>(e1 + v0) = make_uint4(pk[0][0], pk[0][1], pk[1][0], pk[1][1]);
         }
-        const int v0 = m0 + wm * 128 + (2 * ip + (g & 1)) * 16 + (g >> 1) * 8;
-        *reinterpret_cast<uint4*>(e1 + v0) = make_uint4(pk[0][0], pk[0][1], pk[1][0], pk[1][1]);
-      }
-      float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
-      float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
-      ssum += __shfl_xor(ssum, 16, 64);
-      zsum += __shfl_xor(zsum, 16, 64);
-      ssum += __shfl_xor(ssum, 32, 64);
-      zsum += __shfl_xor(zsum, 32, 64);
-      if (g == 0) {
-        xsum[wm * kBN + cl] = ssum;
-        xsz[wm * kBN + cl] = zsum;
+        float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
+        ssum += __shfl_xor(ssum, 16, 64);
+        ssum += __shfl_xor(ssum, 32, 64);
+        if (g == 0) xsum[wm * kBN + cl] = ssum;
+        if constexpr (WZ) {
+          float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
+          zsum += __shfl_xor(zsum, 16, 64);
+          zsum += __shfl_xor(zsum, 32, 64);
+          if (g == 0) xsz[wm * kBN + cl] = zsum;
+        }
+      };
+      if (rows_full) {
+        if (p.psz) pass(std::true_type{}, std::true_type{});
+        else pass(std::true_type{}, std::false_type{});
+      } else {
+        if (p.psz) pass(std::false_type{}, std::true_type{});
+        else pass(std::false_type{}, std::false_type{});
       }
     }
   }
