@@ -12,7 +12,7 @@
 // Work is cut into slabs of whole sequences; per slab:
 //   FWD  C = W . H_slab^T  (rows = vocab, cols = tokens, K = d).  Epilogue: per token,
 //        the block's max and sum exp(z - s_t) over its 256 vocab rows (in-lane over 32
-//        values, two lane shuffles, one LDS exchange), the sampled token's logit, and
+//        values, two lane-row swaps, one LDS exchange), the sampled token's logit, and
 //        E1[t][v] = exp(z - s_t) (s_t = 0 unless exp(z) would leave float range).
 //   merge   partials -> lse, logp, row max; rows whose max is too far from s_t get
 //           s_t = max_t and their token block is evaluated again (rare), then merge again.
@@ -570,13 +570,31 @@ __device__ __forceinline__ void mainloop_f32(const GemmParams& p, int m0, int n0
 }
 
 
+// Reductions over the four 16-lane groups of a wavefront (lanes c, c + 16, c + 32, c + 48) with
+// row swaps instead of LDS-routed shuffles: a 16-lane-row swap of x with itself leaves rows
+// (r0, r0, r2, r2) and (r1, r1, r3, r3), whose sum is the xor-16 partner sum; a half swap then
+// does the same for xor 32.  Each step adds the same two operands as the xor shuffle would.
+__device__ __forceinline__ float group_sum4(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+__device__ __forceinline__ float group_max4(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // Epilogue of the bf16 logits GEMM (16 x 16 accumulator tiles: acc[i][j] covers vocab rows
 // wm*128 + 16 i .. +15 and tokens wn*64 + 16 j .. +15; lane l holds rows 4 (l / 16) + q of
 // token column l % 16).  Per token column: the block's max over its vocab rows, the sampled
 // token's logit, and with a stored exp (store_e != 0) E[t][v] = exp(z - s_t) with the sums
 // sum exp(z - s_t) and sum exp(z - s_t) z; without one (old / ref log-probs), the sums relative
 // to the block max.  A column's 256 rows are spread over the 4 lane groups of two wavefronts:
-// lane shuffles, then one LDS exchange between the wavefronts.
+// lane-row swaps, then one LDS exchange between the wavefronts.
 __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, int n0, int mb,
                                                   f32x4_t (&acc)[8][4], uint16_t* smem) {
   __syncthreads();  // LDS operand buffers are reused for the cross-wave exchange
@@ -599,15 +617,21 @@ __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, i
     const int y = tok_ok ? p.yslab[t] : -1;
     // columns past the slab store exp(z - inf) = 0
     const float s_t = tok_ok ? (p.shift ? p.shift[t] : 0.0f) : INFINITY;
-    // max over the lane's 32 rows in four independent chains
+    // max over the lane's 32 rows in four independent chains; a full vocab block (all but the
+    // last) takes a branch without the row test, so the chains become three-input maxima
     float mxp[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    if (rows_full) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float z = acc[i][j][q];
-        mxp[i & 3] = (rows_full || rbase + 16 * i + q < Vr) ? fmaxf(mxp[i & 3], z) : mxp[i & 3];
-      }
+        for (int q = 0; q < 4; ++q) mxp[i & 3] = fmaxf(mxp[i & 3], acc[i][j][q]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          mxp[i & 3] = fmaxf(mxp[i & 3], rbase + 16 * i + q < Vr ? acc[i][j][q] : -INFINITY);
+    }
     float mx = fmaxf(fmaxf(mxp[0], mxp[1]), fmaxf(mxp[2], mxp[3]));
     // the sampled token's logit: held by one lane group of one wavefront (rare per column)
     const int dy = y - m0 - wm * 128;
@@ -619,8 +643,7 @@ __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, i
         for (int q = 0; q < 4; ++q) zl = (16 * i + q == (dy & ~12)) ? acc[i][j][q] : zl;
       p.zlab[t] = zl;
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    mx = group_max4(mx);
     if (g == 0) xmax[wm * kBN + cl] = mx;
     if (rel) {
       uint16_t* e1 = static_cast<uint16_t*>(p.E1) + int64_t(t) * p.ldE1;
@@ -664,13 +687,11 @@ __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, i
           *reinterpret_cast<uint4*>(e1 + v0) = make_uint4(pk[0][0], pk[0][1], pk[1][0], pk[1][1]);
         }
         float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
-        ssum += __shfl_xor(ssum, 16, 64);
-        ssum += __shfl_xor(ssum, 32, 64);
+        ssum = group_sum4(ssum);
         if (g == 0) xsum[wm * kBN + cl] = ssum;
         if constexpr (WZ) {
           float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
-          zsum += __shfl_xor(zsum, 16, 64);
-          zsum += __shfl_xor(zsum, 32, 64);
+          zsum = group_sum4(zsum);
           if (g == 0) xsz[wm * kBN + cl] = zsum;
         }
       };
@@ -702,10 +723,8 @@ __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, i
         }
       float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
       float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
-      ssum += __shfl_xor(ssum, 16, 64);
-      zsum += __shfl_xor(zsum, 16, 64);
-      ssum += __shfl_xor(ssum, 32, 64);
-      zsum += __shfl_xor(zsum, 32, 64);
+      ssum = group_sum4(ssum);
+      zsum = group_sum4(zsum);
       if (g == 0) {
         xsum[wm * kBN + cl] = ssum;
         xsz[wm * kBN + cl] = zsum;
