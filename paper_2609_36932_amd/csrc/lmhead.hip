@@ -1313,10 +1313,9 @@ __global__ void label_hist_kernel(const int32_t* __restrict__ yslab, int32_t Tc,
   if (t < Tc && yslab[t] >= 0) atomicAdd(&cnt[yslab[t]], 1);
 }
 
-// exclusive scan of cnt[0..n) into off[0..n], cursor = copy of off
+// exclusive scan of cnt[0..n) into off[0..n]
 __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ cnt, int32_t n,
-                                                    int32_t* __restrict__ off,
-                                                    int32_t* __restrict__ cursor) {
+                                                    int32_t* __restrict__ off) {
   __shared__ int32_t ws[16];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   int32_t base = 0;
@@ -1336,68 +1335,215 @@ __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ 
       if (w < wv) pre += ws[w];
       tot += ws[w];
     }
-    if (i < n) {
-      off[i] = base + pre + v - x;
-      cursor[i] = base + pre + v - x;
-    }
+    if (i < n) off[i] = base + pre + v - x;
     base += tot;
     __syncthreads();
   }
   if (tid == 0) off[n] = base;
 }
 
-__global__ void label_fill_kernel(const int32_t* __restrict__ yslab, int32_t Tc,
-                                  int32_t* __restrict__ cursor, int32_t* __restrict__ lab_tok) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < Tc && yslab[t] >= 0) lab_tok[atomicAdd(&cursor[yslab[t]], 1)] = t;
+// ---- label CSR: the slab's labelled tokens ordered by (label, token) ----------------------
+// Keys (label << 32 | token) are sorted with a bitonic network, so the order inside a label
+// is the token order whatever the label distribution (one token id can fill a large part of
+// a slab of real text).  n is a power of two >= kSortTile; unlabelled tokens and the padding
+// carry the largest key and sort to the end.
+constexpr int kSortTile = 2048;  // keys per block in the LDS stages (1024 threads, 16 KB)
+
+__global__ void label_key_kernel(const int32_t* __restrict__ yslab, int32_t Tc, int64_t n,
+                                 uint64_t* __restrict__ key) {
+  const int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
+  if (i >= n) return;
+  const int y = i < Tc ? yslab[i] : -1;
+  key[i] = y >= 0 ? (uint64_t(uint32_t(y)) << 32) | uint64_t(i) : ~uint64_t(0);
 }
 
-// order each label bucket by token index so dW sums in a fixed order
-__global__ void label_sort_kernel(const int32_t* __restrict__ off, int32_t V,
-                                  int32_t* __restrict__ lab_tok) {
-  const int v = blockIdx.x * blockDim.x + threadIdx.x;
-  if (v >= V) return;
-  const int a = off[v], b = off[v + 1];
-  for (int i = a + 1; i < b; ++i) {
-    const int x = lab_tok[i];
-    int j = i - 1;
-    while (j >= a && lab_tok[j] > x) {
-      lab_tok[j + 1] = lab_tok[j];
-      --j;
-    }
-    lab_tok[j + 1] = x;
+// compare-exchange of positions i and i + j inside one LDS tile; the direction of the
+// sequence being built is ascending where bit k of the global position is clear
+__device__ __forceinline__ void bitonic_cx(uint64_t* s, int64_t base, int i, int j, int64_t k) {
+  const uint64_t a = s[i], b = s[i + j];
+  const bool asc = ((base + i) & k) == 0;
+  if (asc ? a > b : a < b) {
+    s[i] = b;
+    s[i + j] = a;
   }
 }
 
+// k_merge == 0: sort every tile (stages k = 2 .. kSortTile); otherwise the steps j < kSortTile
+// of stage k_merge
+__global__ __launch_bounds__(1024) void bitonic_tile_kernel(uint64_t* __restrict__ key,
+                                                            int64_t k_merge) {
+  __shared__ uint64_t s[kSortTile];
+  const int tid = threadIdx.x;
+  const int64_t base = int64_t(blockIdx.x) * kSortTile;
+  s[tid] = key[base + tid];
+  s[tid + kSortTile / 2] = key[base + tid + kSortTile / 2];
+  __syncthreads();
+  auto steps = [&](int64_t k, int j0) {
+    for (int j = j0; j > 0; j >>= 1) {
+      bitonic_cx(s, base, (tid / j) * 2 * j + tid % j, j, k);
+      __syncthreads();
+    }
+  };
+  if (k_merge == 0) {
+    for (int k = 2; k <= kSortTile; k <<= 1) steps(k, k >> 1);
+  } else {
+    steps(k_merge, kSortTile / 2);
+  }
+  key[base + tid] = s[tid];
+  key[base + tid + kSortTile / 2] = s[tid + kSortTile / 2];
+}
+
+// one step j >= kSortTile of stage k, over all n / 2 pairs
+__global__ void bitonic_step_kernel(uint64_t* __restrict__ key, int64_t n, int64_t k, int64_t j) {
+  const int64_t p = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
+  if (p >= n / 2) return;
+  const int64_t i = (p / j) * 2 * j + p % j;
+  const uint64_t a = key[i], b = key[i + j];
+  const bool asc = (i & k) == 0;
+  if (asc ? a > b : a < b) {
+    key[i] = b;
+    key[i + j] = a;
+  }
+}
+
+__global__ void label_tok_kernel(const uint64_t* __restrict__ key, int32_t Tc,
+                                 int32_t* __restrict__ lab_tok) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < Tc && key[i] != ~uint64_t(0)) lab_tok[i] = int32_t(uint32_t(key[i]));
+}
+
 // One-hot part of dW for one slab: dW[v] += sum over the slab tokens t labelled v of g_t H[t],
-// summed in the label CSR's fixed token order (deterministic).  One block per distinct label:
-// the block of the label's first CSR entry does the work, the others exit.
+// as a segmented sum over the label CSR in fixed chunks of kOneHotChunk positions (one block
+// per chunk, four consecutive columns per thread).  A label whose tokens all lie in the chunk
+// is added to dW by the chunk; a label cut by a chunk edge leaves its chunk partials (the part
+// after the edge in `head`, the part before it in `tail`) for dw_onehot_carry_kernel, which
+// adds them in chunk order.  Every sum has a fixed order, so dW is deterministic, and the work
+// per block is bounded however the labels are distributed.
+constexpr int kOneHotChunk = 128;
+
+template <typename T>
+__device__ __forceinline__ void load4(const T* p, float (&v)[4]);
+template <>
+__device__ __forceinline__ void load4<uint16_t>(const uint16_t* p, float (&v)[4]) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  v[0] = __uint_as_float(u.x << 16);
+  v[1] = __uint_as_float(u.x & 0xffff0000u);
+  v[2] = __uint_as_float(u.y << 16);
+  v[3] = __uint_as_float(u.y & 0xffff0000u);
+}
+template <>
+__device__ __forceinline__ void load4<float>(const float* p, float (&v)[4]) {
+  const float4 u = *reinterpret_cast<const float4*>(p);
+  v[0] = u.x;
+  v[1] = u.y;
+  v[2] = u.z;
+  v[3] = u.w;
+}
+
+__device__ __forceinline__ void add4(float* __restrict__ p, const float (&s)[4]) {
+  float4 w = *reinterpret_cast<float4*>(p);
+  w.x += s[0];
+  w.y += s[1];
+  w.z += s[2];
+  w.w += s[3];
+  *reinterpret_cast<float4*>(p) = w;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void dw_onehot_kernel(
     const int32_t* __restrict__ lab_off, const int32_t* __restrict__ lab_tok,
     const int32_t* __restrict__ yslab, const float* __restrict__ gslab, const T* __restrict__ H,
     const int32_t* __restrict__ row_index, int64_t row_base, int32_t d, int32_t V,
-    float* __restrict__ dW) {
-  const int e = blockIdx.x;
-  if (e >= lab_off[V]) return;
-  const int y = yslab[lab_tok[e]];
-  const int a = lab_off[y], b = lab_off[y + 1];
-  if (a != e) return;
-  // four consecutive columns per thread (d is a multiple of 8), their loads independent
+    float* __restrict__ dW, float* __restrict__ head, float* __restrict__ tail) {
+  __shared__ int64_t srow[kOneHotChunk];
+  __shared__ float sg[kOneHotChunk];
+  __shared__ int32_t sy[kOneHotChunk], sflag[kOneHotChunk];
+  const int nvalid = lab_off[V];
+  const int lo = blockIdx.x * kOneHotChunk;
+  if (lo >= nvalid) return;
+  const int cnt = min(kOneHotChunk, nvalid - lo), hi = lo + cnt;
+  for (int i = threadIdx.x; i < cnt; i += blockDim.x) {
+    const int t = lab_tok[lo + i];
+    const int y = yslab[t];
+    int64_t row = row_base + t;
+    if (row_index) row = row_index[row];
+    srow[i] = row;
+    sg[i] = gslab[t];
+    sy[i] = y;
+    // bit 0: last position of its label in the chunk; bit 1: the label starts in the chunk;
+    // bit 2: it ends in the chunk
+    const bool last = i + 1 == cnt || yslab[lab_tok[lo + i + 1]] != y;
+    sflag[i] = (last ? 1 : 0) | (lab_off[y] >= lo ? 2 : 0) | (lab_off[y + 1] <= hi ? 4 : 0);
+  }
+  __syncthreads();
+  // U positions per batch: their H rows, and the dW rows of the labels that end inside the
+  // chunk at them, are loaded before any of them is used (with one label per position, as
+  // in a near-uniform distribution, every position ends a label)
+  constexpr int U = 8;
   for (int n0 = threadIdx.x * 4; n0 < d; n0 += blockDim.x * 4) {
     float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int i = a; i < b; ++i) {
-      const int t = lab_tok[i];
-      int64_t row = row_base + t;
-      if (row_index) row = row_index[row];
-      const float g = gslab[t];
-      const T* h = H + row * d + n0;
+    for (int i0 = 0; i0 < cnt; i0 += U) {
+      float h[U][4], w[U][4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s[q] += g * to_f32<T>(h[q]);
+      for (int u = 0; u < U; ++u)
+        if (i0 + u < cnt) {
+          load4<T>(H + srow[i0 + u] * d + n0, h[u]);
+          if (sflag[i0 + u] == 7) load4<float>(dW + int64_t(sy[i0 + u]) * d + n0, w[u]);
+        }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u;
+        if (i >= cnt) break;
+        const float g = sg[i];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s[q] += g * h[u][q];
+        const int f = sflag[i];
+        if (f & 1) {
+          if (f == 7) {
+            *reinterpret_cast<float4*>(dW + int64_t(sy[i]) * d + n0) =
+                make_float4(w[u][0] + s[0], w[u][1] + s[1], w[u][2] + s[2], w[u][3] + s[3]);
+          } else {
+            float* c = ((f & 2) ? tail : head) + int64_t(blockIdx.x) * d + n0;
+            *reinterpret_cast<float4*>(c) = make_float4(s[0], s[1], s[2], s[3]);
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) s[q] = 0.0f;
+        }
+      }
     }
-    float* w = dW + int64_t(y) * d + n0;
+  }
+}
+
+// labels cut by chunk edges: the chunk where such a label starts adds its own tail partial and
+// the head partials of the following chunks up to the one where the label ends
+__global__ __launch_bounds__(256) void dw_onehot_carry_kernel(
+    const int32_t* __restrict__ lab_off, const int32_t* __restrict__ lab_tok,
+    const int32_t* __restrict__ yslab, int32_t d, int32_t V, float* __restrict__ dW,
+    const float* __restrict__ head, const float* __restrict__ tail) {
+  const int nvalid = lab_off[V];
+  const int lo = blockIdx.x * kOneHotChunk;
+  if (lo >= nvalid) return;
+  const int hi = min(lo + kOneHotChunk, nvalid);
+  const int y = yslab[lab_tok[hi - 1]];
+  const int a = lab_off[y], b = lab_off[y + 1];
+  if (a < lo || b <= hi) return;  // the chunk's last label starts before it or ends in it
+  const int c1 = (b - 1) / kOneHotChunk;
+  for (int n0 = threadIdx.x * 4; n0 < d; n0 += blockDim.x * 4) {
+    float s[4];
+    load4<float>(tail + int64_t(blockIdx.x) * d + n0, s);
+    for (int c0 = blockIdx.x + 1; c0 <= c1; c0 += 8) {  // 8 loads in flight, added in order
+      float h[8][4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) w[q] += s[q];
+      for (int u = 0; u < 8; ++u)
+        if (c0 + u <= c1) load4<float>(head + int64_t(c0 + u) * d + n0, h[u]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (c0 + u <= c1) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) s[q] += h[u][q];
+        }
+    }
+    add4(dW + int64_t(y) * d + n0, s);
   }
 }
 
@@ -1548,9 +1694,18 @@ static SlabPlan plan_slabs(const int64_t* off, int32_t S, int64_t cap) {
 struct LossWs {
   void *WT, *E1, *Bd;
   float *pmax, *psum, *psz, *ent, *zlab, *shift, *gslab, *cslab, *lse, *logp;
-  int32_t *yslab, *redo_blk, *redo_count, *seq_clip, *lab_cnt, *lab_off, *lab_cur, *lab_tok;
+  int32_t *yslab, *redo_blk, *redo_count, *seq_clip, *lab_cnt, *lab_off, *lab_tok;
+  uint64_t* lab_key;
+  float *oh_head, *oh_tail;
   double* seq_loss;
 };
+
+// length of the label sort: a power of two >= max(n, kSortTile)
+static int64_t sort_len(int64_t n) {
+  int64_t m = kSortTile;
+  while (m < n) m <<= 1;
+  return m;
+}
 
 static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_t tc_max) {
   const int esz = a.dtype == FASTRL_BF16 ? 2 : 4;
@@ -1580,8 +1735,11 @@ static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_
   w.seq_clip = c.take<int32_t>(size_t(std::max(a.S, 1)));
   w.lab_cnt = c.take<int32_t>(size_t(a.V + 1));
   w.lab_off = c.take<int32_t>(size_t(a.V + 1));
-  w.lab_cur = c.take<int32_t>(size_t(a.V + 1));
   w.lab_tok = c.take<int32_t>(size_t(tcp));
+  w.lab_key = dw ? c.take<uint64_t>(size_t(sort_len(tcp))) : nullptr;
+  const int64_t nch = (tcp + kOneHotChunk - 1) / kOneHotChunk;
+  w.oh_head = dw ? c.take<float>(size_t(nch * a.d)) : nullptr;
+  w.oh_tail = dw ? c.take<float>(size_t(nch * a.d)) : nullptr;
   return c.size();
 }
 
@@ -1695,15 +1853,30 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
       hipLaunchKernelGGL(label_hist_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0,
                          stream, w.yslab, Tc, w.lab_cnt);
       FR_LAUNCHED();
-      hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, w.lab_cnt, V, w.lab_off,
-                         w.lab_cur);
+      hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, w.lab_cnt, V, w.lab_off);
       FR_LAUNCHED();
-      hipLaunchKernelGGL(label_fill_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0,
-                         stream, w.yslab, Tc, w.lab_cur, w.lab_tok);
-      FR_LAUNCHED();
-      hipLaunchKernelGGL(label_sort_kernel, dim3(nb1d(V, 256)), dim3(256), 0, stream,
-                         w.lab_off, V, w.lab_tok);
-      FR_LAUNCHED();
+      if (Tc > 0) {  // label CSR in (label, token) order: bitonic sort of the slab's keys
+        const int64_t n = sort_len(Tc);
+        hipLaunchKernelGGL(label_key_kernel, dim3(unsigned(n / 256)), dim3(256), 0, stream,
+                           w.yslab, Tc, n, w.lab_key);
+        FR_LAUNCHED();
+        hipLaunchKernelGGL(bitonic_tile_kernel, dim3(unsigned(n / kSortTile)), dim3(1024), 0,
+                           stream, w.lab_key, int64_t(0));
+        FR_LAUNCHED();
+        for (int64_t k = 2 * kSortTile; k <= n; k <<= 1) {
+          for (int64_t j = k / 2; j >= kSortTile; j >>= 1) {
+            hipLaunchKernelGGL(bitonic_step_kernel, dim3(unsigned(n / 2 / 256)), dim3(256), 0,
+                               stream, w.lab_key, n, k, j);
+            FR_LAUNCHED();
+          }
+          hipLaunchKernelGGL(bitonic_tile_kernel, dim3(unsigned(n / kSortTile)), dim3(1024), 0,
+                             stream, w.lab_key, k);
+          FR_LAUNCHED();
+        }
+        hipLaunchKernelGGL(label_tok_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream,
+                           w.lab_key, Tc, w.lab_tok);
+        FR_LAUNCHED();
+      }
       GemmParams q{};
       q.K = int32_t(Tr);
       q.dW = a.dW; q.dW_acc = (si > 0 || a.dW_accumulate) ? 1 : 0;
@@ -1719,9 +1892,13 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
         FR_TRY((launch_gemm<T, MODE_DW>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
       }
       if (Tc > 0) {
-        hipLaunchKernelGGL((dw_onehot_kernel<T>), dim3(unsigned(Tc)), dim3(256), 0, stream,
-                           w.lab_off, w.lab_tok, w.yslab, w.gslab, static_cast<const T*>(a.hidden),
-                           a.row_index, t0, d, V, a.dW);
+        const unsigned nch = unsigned((Tc + kOneHotChunk - 1) / kOneHotChunk);
+        hipLaunchKernelGGL((dw_onehot_kernel<T>), dim3(nch), dim3(256), 0, stream, w.lab_off,
+                           w.lab_tok, w.yslab, w.gslab, static_cast<const T*>(a.hidden),
+                           a.row_index, t0, d, V, a.dW, w.oh_head, w.oh_tail);
+        FR_LAUNCHED();
+        hipLaunchKernelGGL(dw_onehot_carry_kernel, dim3(nch), dim3(256), 0, stream, w.lab_off,
+                           w.lab_tok, w.yslab, d, V, a.dW, w.oh_head, w.oh_tail);
         FR_LAUNCHED();
       }
     }

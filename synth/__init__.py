@@ -218,3 +218,14 @@ def plant_duplicates(ro, p_copy=0.6, p_mutate=0.15, seed=7):
             t[m] = rng.integers(0, V, size=int(m.sum()))
             ro.token_ids[s0:s1] = t
     return ro
+
+
+def skew_tokens(ro, frac, token=0, seed=11):
+    """Test-only structure: a head-heavy token distribution, as in real text where a few ids
+    (spaces, punctuation, end of text) fill a large share of the positions.  Each position
+    becomes ``token`` with probability ``frac`` (1.0: every position).  Modifies
+    ``ro.token_ids`` in place."""
+    rng = _rng(seed, 98)
+    m = rng.uniform(size=ro.token_ids.shape[0]) < frac
+    ro.token_ids[m] = token
+    return ro

@@ -8,7 +8,7 @@ import numpy as np
 import torch
 
 import oracle
-from synth import CONFIGS, make_rollouts, make_dense, plant_duplicates
+from synth import CONFIGS, make_rollouts, make_dense, plant_duplicates, skew_tokens
 
 LOGP_ATOL = 2e-3
 REL = 1e-2
@@ -32,7 +32,7 @@ class Problem:
 
     def __init__(self, cfg_id, dev, *, Q=None, len_range=None, G=None, V=None, d=None,
                  dtype=None, seed=None, h_std=1.0, w_std=0.02, ngram_n=None, keep_ratio=None,
-                 tau=None, vocab_ids=None, planted=None):
+                 tau=None, vocab_ids=None, planted=None, skew=None):
         base = CONFIGS[cfg_id]
         self.cfg = base
         self.V = V or base.V
@@ -44,6 +44,8 @@ class Problem:
         ro = make_rollouts(base, seed=seed, Q=Q, len_range=len_range, G=G, V=vocab_ids or self.V)
         if planted is not None:
             plant_duplicates(ro, **planted)
+        if skew is not None:
+            skew_tokens(ro, skew)
         self.ro = ro
         self.dev = dev
         pr = oracle.hot_path_step(ro.rewards, ro.group_off, ro.token_ids, ro.traj_tok_off,

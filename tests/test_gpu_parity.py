@@ -220,6 +220,27 @@ def test_deterministic(fr):
     assert torch.equal(a["call"].dhidden, b["call"].dhidden)
 
 
+@pytest.mark.parametrize("skew", [0.7, 1.0])
+@pytest.mark.parametrize("slab", [0, 1000])
+def test_head_heavy_labels(fr, skew, slab):
+    """A token distribution where one id fills most positions (1.0: all of them): the label
+    with thousands of tokens crosses many chunks of the one-hot dW sum.  dW matches the
+    oracle and is the same bit for bit on a second run."""
+    pb = Problem(3, DEV, Q=8, len_range=(60, 200), V=500, d=64, skew=skew)
+    ref = pb.oracle_loss()
+    st = _status()
+    a = pb.run_gpu(fr, slab_tokens=slab, status=st)
+    b = pb.run_gpu(fr, slab_tokens=slab)
+    torch.cuda.synchronize()
+    assert st.item() == 0, fr.status_names(st.item())
+    T = a["t_kept"]
+    assert T == len(pb.src) and int((pb.y == 0).sum()) > 2000
+    call = a["call"]
+    check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
+                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"])
+    assert torch.equal(call.dW, b["call"].dW)
+
+
 def test_empty_and_single_token(fr):
     # no kept sequence at all: loss 0, dW zero
     d, V = 64, 300

@@ -5,7 +5,8 @@ import math
 import numpy as np
 import pytest
 
-from synth import CONFIGS, make_rollouts, make_dense, TOKEN_EDGE_MARGIN, SEQ_EDGE_MARGIN
+from synth import (CONFIGS, make_rollouts, make_dense, skew_tokens, TOKEN_EDGE_MARGIN,
+                   SEQ_EDGE_MARGIN)
 
 
 @pytest.mark.parametrize("c", [1, 2, 3])
@@ -49,3 +50,13 @@ def test_dense_deterministic_small():
     assert H1.dtype == torch.float32 and W1.shape == (50, 32)
     Hb, Wb = make_dense(CONFIGS[2], 10, d=16, V=8)
     assert Hb.dtype == torch.bfloat16
+
+
+def test_skew_tokens_head_share():
+    a = skew_tokens(make_rollouts(CONFIGS[3], Q=8), 0.7)
+    b = skew_tokens(make_rollouts(CONFIGS[3], Q=8), 0.7)
+    assert np.array_equal(a.token_ids, b.token_ids)
+    share = float((a.token_ids == 0).mean())
+    assert 0.68 < share < 0.72, share
+    c = skew_tokens(make_rollouts(CONFIGS[3], Q=2), 1.0)
+    assert (c.token_ids == 0).all()
