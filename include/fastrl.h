@@ -357,7 +357,8 @@ int fastrl_ars_observe(fastrl_ars_state* st, const int32_t* counts_host,
  * Kernel timing (for benchmarks).  While enabled, every launch of the dominant kernels is
  * bracketed by HIP events on the launch stream; fastrl_profile_read synchronises those
  * events and returns the summed duration (ms), the launch count and the algorithmic
- * FLOPs of the launches of one kernel kind.  Not thread-safe; off by default.
+ * FLOPs of the launches of one kernel kind.  Off by default.  The recorder is one
+ * process-wide list behind a lock: launches from every thread and stream are summed.
  * ------------------------------------------------------------------------------------ */
 typedef enum fastrl_kernel_kind {
   FASTRL_K_LOGITS_FWD = 0,  /* logits GEMM + online log-sum-exp epilogue        */

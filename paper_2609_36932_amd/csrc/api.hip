@@ -1,5 +1,6 @@
 // C ABI of libfastrl: argument validation, error text, workspace queries, kernel timing,
 // and the host-only Adaptive Rollout Sampling controller (Sec. 3.3; Alg. 1 Phase 1).
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <mutex>
@@ -37,7 +38,8 @@ struct ProfRec {
   double flops;
   hipEvent_t a, b;
 };
-static bool g_prof_on = false;
+static std::atomic<bool> g_prof_on{false};
+static std::mutex g_prof_mu;  // guards g_prof and g_ev_pool
 static std::vector<ProfRec> g_prof;
 static std::vector<hipEvent_t> g_ev_pool;
 
@@ -53,12 +55,14 @@ static hipEvent_t take_event() {
 }
 
 ProfScope::ProfScope(int k, hipStream_t s, double f) : kind(k), stream(s), flops(f) {
-  if (!g_prof_on || k < 0) return;
+  if (!g_prof_on.load(std::memory_order_relaxed) || k < 0) return;
+  std::lock_guard<std::mutex> lock(g_prof_mu);
   hipEvent_t e = take_event();
   if (e && hipEventRecord(e, s) == hipSuccess) ev0 = e;
 }
 ProfScope::~ProfScope() {
   if (!ev0) return;
+  std::lock_guard<std::mutex> lock(g_prof_mu);
   hipEvent_t e = take_event();
   if (e && hipEventRecord(e, stream) == hipSuccess)
     g_prof.push_back(ProfRec{kind, flops, static_cast<hipEvent_t>(ev0), e});
@@ -331,11 +335,12 @@ int fastrl_ars_observe(fastrl_ars_state* st, const int32_t* counts_host,
 
 // ---- kernel timing ---------------------------------------------------------------------
 int fastrl_profile_enable(int32_t on) {
-  g_prof_on = on != 0;
+  g_prof_on.store(on != 0, std::memory_order_relaxed);
   return FASTRL_OK;
 }
 
 int fastrl_profile_reset(void) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
   for (auto& r : g_prof) {
     g_ev_pool.push_back(r.a);
     g_ev_pool.push_back(r.b);
@@ -350,6 +355,7 @@ int fastrl_profile_read(int32_t kind, double* total_ms, int64_t* launches, doubl
                "fastrl_profile_read: NULL output");
   double ms = 0.0, fl = 0.0;
   int64_t n = 0;
+  std::lock_guard<std::mutex> lock(g_prof_mu);
   for (auto& r : g_prof) {
     if (r.kind != kind) continue;
     FR_HIP(hipEventSynchronize(r.b));

@@ -1313,19 +1313,26 @@ __global__ void label_hist_kernel(const int32_t* __restrict__ yslab, int32_t Tc,
   if (t < Tc && yslab[t] >= 0) atomicAdd(&cnt[yslab[t]], 1);
 }
 
-// exclusive scan of cnt[0..n) into off[0..n]
+// exclusive scan of cnt[0..n) into off[0..n]: one block, 8 consecutive counts per thread, so
+// a pass covers 8192 counts (19 passes at a 152K vocabulary)
 __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ cnt, int32_t n,
                                                     int32_t* __restrict__ off) {
+  constexpr int E = 8;
   __shared__ int32_t ws[16];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   int32_t base = 0;
-  for (int c = 0; c < n; c += 1024) {
-    const int i = c + tid;
-    const int x = i < n ? cnt[i] : 0;
-    int v = x;
+  for (int c = 0; c < n; c += 1024 * E) {
+    const int i0 = c + tid * E;
+    int x[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) x[e] = i0 + e < n ? cnt[i0 + e] : 0;
+    int tsum = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) tsum += x[e];
+    int v = tsum;  // inclusive scan of the thread sums over the wavefront
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      int t = __shfl_up(v, o, 64);
+      const int t = __shfl_up(v, o, 64);
       if (lane >= o) v += t;
     }
     if (lane == 63) ws[wv] = v;
@@ -1335,7 +1342,12 @@ __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ 
       if (w < wv) pre += ws[w];
       tot += ws[w];
     }
-    if (i < n) off[i] = base + pre + v - x;
+    int run = base + pre + v - tsum;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      if (i0 + e < n) off[i0 + e] = run;
+      run += x[e];
+    }
     base += tot;
     __syncthreads();
   }
