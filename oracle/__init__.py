@@ -28,7 +28,7 @@ from .advantage import group_advantage
 from .mdap import (ngram_set, jaccard_counts, theta_below_tau, greedy_mdap_class,
                    budget_keep, prune_prompt, prune_batch, compact, continuous_classes,
                    visit_order, dp_align_fill)
-from .lmhead import token_logprob, lmhead_backward, logits, token_entropy
+from .lmhead import token_logprob, lmhead_backward, lmhead_dW_rows, logits, token_entropy
 from .loss import policy_loss, token_weights
 from .ars import ARSController
 from .optim import adamw_step
@@ -38,7 +38,7 @@ __all__ = [
     "group_advantage", "ngram_set", "jaccard_counts", "theta_below_tau",
     "greedy_mdap_class", "budget_keep", "prune_prompt", "prune_batch", "compact",
     "continuous_classes", "visit_order", "dp_align_fill",
-    "token_logprob", "lmhead_backward", "logits", "token_entropy", "policy_loss",
+    "token_logprob", "lmhead_backward", "lmhead_dW_rows", "logits", "token_entropy", "policy_loss",
     "token_weights",
     "ARSController", "hot_path_step", "adamw_step",
 ]

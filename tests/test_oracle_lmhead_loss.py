@@ -233,3 +233,40 @@ def test_autograd_crosscheck():
     assert abs(tl.item() - loss) < 1e-12
     np.testing.assert_allclose(Ht.grad.numpy(), dH, atol=1e-12)
     np.testing.assert_allclose(Wt.grad.numpy(), dW, atol=1e-12)
+
+
+def test_dW_rows_match_full_backward_and_finite_differences():
+    """lmhead_dW_rows (exact dW rows for chosen vocabulary ids, used where the full dW is
+    too large to form) equals the rows of the full backward, for ids that are labels, ids
+    that are not, repeated ids and any chunking; and its rows are the central finite
+    differences of the composite loss w.r.t. those rows of W."""
+    from oracle.lmhead import lmhead_dW_rows
+    rng = np.random.default_rng(13)
+    S, d, V = 5, 12, 40
+    L = rng.integers(2, 7, size=S)
+    off = np.concatenate([[0], np.cumsum(L)])
+    T = off[-1]
+    H = rng.normal(size=(T, d))
+    W = rng.normal(scale=0.3, size=(V, d))
+    y = rng.integers(0, V // 2, size=T)  # the upper half of the vocabulary is never a label
+    A = rng.normal(size=S)
+    x, lse = token_logprob(H, W, y)
+    o = x + rng.choice([-0.5, -0.05, 0.05, 0.5], size=T)
+    f = x + rng.normal(0, 0.2, size=T)
+    kw = dict(algo="grpo", norm="seq_mean_token_mean", eps_low=0.2, eps_high=0.2, beta=0.04)
+    _, g, _ = policy_loss(x, o, f, off, A, **kw)
+    _, dW = lmhead_backward(H, W, y, lse, g)
+    rows = np.asarray([int(y[0]), int(y[3]), V - 1, V // 2 + 1, int(y[0]), 0])
+    for chunk in (1, 3, T, 4096):
+        got = lmhead_dW_rows(H, W, y, lse, g, rows, row_chunk=chunk)
+        np.testing.assert_allclose(got, dW[rows], rtol=0, atol=1e-14)
+    got = lmhead_dW_rows(H, W, y, lse, g, rows)
+    h = 1e-6
+    for r, v in enumerate(rows[:4]):
+        for k in rng.choice(d, size=3, replace=False):
+            Wp, Wm = W.copy(), W.copy()
+            Wp[v, k] += h
+            Wm[v, k] -= h
+            fd = (_composite(H, Wp, y, o, f, off, A, **kw) -
+                  _composite(H, Wm, y, o, f, off, A, **kw)) / (2 * h)
+            assert abs(fd - got[r, k]) < 1e-6 * max(1e-3, abs(got[r, k])) + 1e-9, (v, k)
