@@ -249,15 +249,17 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
  *   training, Sec. 4), accumulated in the same pass as the log-sum-exp (one more partial
  *   sum exp(z - s_t) z per vocabulary block).  entropy_sum [1] float (may be NULL): sum_t H_t
  *   in float64, fixed order (the mean entropy is entropy_sum / T).
- * Limits: d % 8 == 0; hidden, W and dW 16-byte aligned (FASTRL_ERR_VALUE); S >= 0; every
- *   sequence no longer than the slab (slab_tokens; 0 picks the largest slab whose exp-logit
- *   buffer stays within 48 GiB, ~169K tokens at V = 152064 in bf16; a longer sequence raises
- *   the slab to its length).  The tokens are spread over ceil(T / slab_tokens) slabs of about
- *   equal size.
- * The work runs slab by slab; each slab stores exp(z - s_t) (s_t = 0, or the row max when
- * exp(z) would leave float range) for its tokens in the workspace, so the workspace holds
- * slab * V_pad * sizeof(dtype) bytes (V_pad = V rounded up to 256), W^T (d * V_pad) when
- * dhidden is wanted, and small per-token and per-(vocabulary block, token) arrays.
+ * Limits: d % 8 == 0; hidden, W and dW 16-byte aligned (FASTRL_ERR_VALUE); S >= 0;
+ *   slab_tokens >= 0 (FASTRL_ERR_VALUE).
+ * Slabs: the work runs in slabs of whole sequences.  slab_tokens is the target slab size
+ *   (0 = 32768 tokens, whatever T is); each slab takes an even share of the tokens left
+ *   (ceil(left / slab_tokens) slabs to go, recounted after every slab) and never holds more
+ *   than max(1.25 slab_tokens, longest sequence) tokens.  Each slab stores exp(z - s_t)
+ *   (s_t = 0, or the row max when exp(z) would leave float range) for its tokens in the
+ *   workspace, so the [T, V] logits are never stored: the workspace holds
+ *   slab * V_pad * sizeof(dtype) bytes (V_pad = V rounded up to 256; 10 GB for the default
+ *   slab at V = 152064 in bf16), W^T (d * V_pad) when dhidden is wanted, and small per-token
+ *   and per-(vocabulary block, token) arrays.
  * ------------------------------------------------------------------------------------ */
 typedef struct fastrl_loss_args {
   const void* hidden;
@@ -300,6 +302,15 @@ typedef struct fastrl_loss_args {
 size_t fastrl_loss_args_size(void);
 size_t fastrl_policy_loss_workspace_size(const fastrl_loss_args* args);
 int fastrl_policy_loss_fwd_bwd(const fastrl_loss_args* args, hipStream_t stream);
+
+/* fastrl_policy_loss_slab_plan -- the slabs fastrl_policy_loss_fwd_bwd runs for these
+ * arguments (host only: reads S, T, seq_off_host and slab_tokens; validates like the call
+ * itself, without the workspace).  Returns the slab count n >= 0 (0 when S == 0) or a
+ * negative fastrl_status.  *max_slab_tokens (may be NULL) receives the largest slab's token
+ * count; when seq_begin_host is not NULL and capacity > n, seq_begin_host[0..n] receives the
+ * first sequence of each slab followed by S (with a smaller capacity nothing is written). */
+int fastrl_policy_loss_slab_plan(const fastrl_loss_args* args, int32_t* seq_begin_host,
+                                 int32_t capacity, int64_t* max_slab_tokens);
 
 /* ------------------------------------------------------------------------------------
  * fastrl_adamw_step -- the policy update that consumes dW (Alg. 1, "update pi_theta"; the

@@ -89,6 +89,8 @@ _SIGS = {
     "fastrl_loss_args_size": (_sz, []),
     "fastrl_policy_loss_workspace_size": (_sz, [ctypes.POINTER(LossArgs)]),
     "fastrl_policy_loss_fwd_bwd": (ctypes.c_int, [ctypes.POINTER(LossArgs), _vp]),
+    "fastrl_policy_loss_slab_plan": (ctypes.c_int, [ctypes.POINTER(LossArgs), _vp, _i32,
+                                                    ctypes.POINTER(_i64)]),
     "fastrl_adamw_step": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _f32, _f32,
                                          _f32, _f32, _f32, _f32, _vp, _vp]),
     "fastrl_ars_init": (ctypes.c_int, [ctypes.POINTER(ARSState), _i32, _i64, _i64]),
@@ -334,6 +336,21 @@ class LossCall:
         _check(_lib.fastrl_policy_loss_fwd_bwd(ctypes.byref(self.args), _stream()),
                "fastrl_policy_loss_fwd_bwd")
         return self
+
+    def slab_plan(self):
+        """(first sequence of each slab followed by S, largest slab's token count)."""
+        return slab_plan(self.args)
+
+
+def slab_plan(args):
+    """The slabs fastrl_policy_loss_fwd_bwd runs for a LossArgs (host only): returns
+    (list of each slab's first sequence followed by S, largest slab's token count)."""
+    tc = _i64()
+    n = _lib.fastrl_policy_loss_slab_plan(ctypes.byref(args), None, 0, ctypes.byref(tc))
+    _check(min(n, 0), "fastrl_policy_loss_slab_plan")
+    buf = (ctypes.c_int32 * (n + 1))()
+    _lib.fastrl_policy_loss_slab_plan(ctypes.byref(args), buf, n + 1, None)
+    return list(buf), tc.value
 
 
 def policy_loss_fwd_bwd(*args, **kw):

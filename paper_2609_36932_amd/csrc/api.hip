@@ -23,6 +23,8 @@ size_t token_logprob_workspace(int64_t T, int32_t d, int32_t V, int32_t dtype);
 int run_token_logprob(const void*, const int32_t*, const void*, int32_t, int64_t, int32_t,
                       int32_t, const int32_t*, float*, float*, int32_t*, void*, hipStream_t);
 size_t policy_loss_workspace(const fastrl_loss_args& a);
+int policy_loss_slab_plan(const fastrl_loss_args& a, int32_t* seq_begin, int32_t capacity,
+                          int64_t* tc_max);
 int launch_adamw(float* theta, uint16_t* wbf, const float* grad, float* mom, float* var,
                  int64_t n, int64_t step, float lr, float beta1, float beta2, float eps,
                  float weight_decay, float grad_scale, int32_t* status, hipStream_t stream);
@@ -230,6 +232,7 @@ static int check_loss_args(const fastrl_loss_args* a, bool need_ws) {
                    a->eps_high >= 0 && a->eps_low < 1,
                FASTRL_ERR_VALUE, "fastrl_policy_loss: need 0 <= eps_low < 1, eps_high >= 0");
   FR_CHECK_ARG(std::isfinite(a->beta), FASTRL_ERR_VALUE, "fastrl_policy_loss: beta not finite");
+  FR_CHECK_ARG(a->slab_tokens >= 0, FASTRL_ERR_VALUE, "fastrl_policy_loss: slab_tokens < 0");
   FR_CHECK_ARG(a->seq_off_host && a->seq_off && a->loss, FASTRL_ERR_NULL_PTR,
                "fastrl_policy_loss: seq_off / seq_off_host / loss is NULL");
   FR_CHECK_ARG(a->seq_off_host[0] == 0 && a->seq_off_host[a->S] == a->T, FASTRL_ERR_SHAPE,
@@ -263,6 +266,14 @@ size_t fastrl_policy_loss_workspace_size(const fastrl_loss_args* args) {
   clear_error();
   if (check_loss_args(args, false) != FASTRL_OK) return 0;
   return policy_loss_workspace(*args);
+}
+
+int fastrl_policy_loss_slab_plan(const fastrl_loss_args* args, int32_t* seq_begin_host,
+                                 int32_t capacity, int64_t* max_slab_tokens) {
+  clear_error();
+  const int rc = check_loss_args(args, false);
+  if (rc != FASTRL_OK) return rc;
+  return policy_loss_slab_plan(*args, seq_begin_host, capacity, max_slab_tokens);
 }
 
 int fastrl_policy_loss_fwd_bwd(const fastrl_loss_args* args, hipStream_t stream) {

@@ -23,7 +23,8 @@
 //        reads): bf16 computes C' = Bd . E1 (rows = d, cols = vocab), f32 computes
 //        C = E1^T . Bd^T (rows = vocab, cols = d):
 //        dW[v] (+)= -C[v] + sum_{t in slab, y_t = v} g_t H[t].
-// Nothing of size [T, V] exists; the slab buffers hold [slab, V].
+// Nothing of size [T, V] exists: the exp-logit buffer holds one slab, [slab, V], and the
+// default slab (32768 tokens) does not grow with T.
 #include <algorithm>
 #include <cstdlib>
 #include <vector>
@@ -1661,43 +1662,42 @@ int run_token_logprob(const void* hidden, const int32_t* row_index, const void* 
 }
 
 // ---------------------------------------------------------------- loss forward/backward
-// Default slab: the largest whose exp-logit buffer [slab, V_pad] stays within 48 GiB of the
-// 288 GB of HBM (at V = 152064 in bf16, ~169K tokens); a caller bounds the workspace with
-// slab_tokens.  Fewer, larger slabs launch fewer GEMMs and skip the read-modify-write of dW
-// between slabs.
-constexpr int64_t kDefaultSlabBytes = int64_t(48) << 30;
+// Default slab: 32768 tokens whatever T is, so the exp-logit buffer [slab, V_pad] is bounded
+// (10 GB in bf16 at V = 152064) and no [T, V] array exists for any T; a caller picks another
+// bound with slab_tokens.
+constexpr int64_t kDefaultSlabTokens = 32768;
 
 struct SlabPlan {
   std::vector<int32_t> seq_begin;  // first sequence of each slab; back() == S
   int64_t tc_max = 0;
 };
 
-// Whole sequences per slab; the T tokens go into nslab = ceil(T / cap) slabs of about
-// T / nslab tokens each (each slab ends at the sequence boundary closest to an even share of
-// what is left, never past 1.25 cap unless one sequence is longer), so the last slab is not
-// a small remainder that leaves most of the GPU idle.
+// Whole sequences per slab.  Each slab takes an even share of what is left, counted afresh
+// after every slab (ceil(remaining / cap) slabs to go, so the shares stay close to cap): it
+// ends at the sequence boundary closest to that share, never past 1.25 cap unless a single
+// sequence is longer, so every slab holds at most max(1.25 cap, longest sequence) tokens.
+// A slab holds at least one token while any are left (empty sequences join the slab of
+// their neighbours); only T == 0 gives a slab without tokens.
 static SlabPlan plan_slabs(const int64_t* off, int32_t S, int64_t cap) {
   SlabPlan pl;
-  const int64_t T = S > 0 ? off[S] - off[0] : 0;
-  const int64_t nslab = std::max<int64_t>(1, (T + cap - 1) / cap);
   const int64_t hard = cap + cap / 4;
   int32_t i = 0;
-  int64_t k = 0;
   while (i < S) {
     pl.seq_begin.push_back(i);
     const int64_t start = off[i];
-    const int64_t left = nslab - k > 1 ? nslab - k : 1;
-    const int64_t target = (off[S] - start + left - 1) / left;
-    int32_t best = i + 1;
-    if (left == 1) {
-      best = S;
-    } else {
-      for (int32_t j = i + 2; j <= S && off[j] - start <= hard; ++j)
+    const int64_t rem = off[S] - start;
+    const int64_t left = std::max<int64_t>(1, (rem + cap - 1) / cap);
+    int32_t best = S;
+    if (left > 1) {
+      const int64_t target = (rem + left - 1) / left;
+      best = i + 1;
+      while (best < S && off[best] == start) ++best;  // at least one token
+      for (int32_t j = best + 1; j <= S && off[j] - start <= hard; ++j)
         if (std::llabs(off[j] - start - target) < std::llabs(off[best] - start - target)) best = j;
+      while (best < S && off[best + 1] == off[best]) ++best;  // trailing empty sequences
     }
     pl.tc_max = std::max<int64_t>(pl.tc_max, off[best] - start);
     i = best;
-    ++k;
   }
   pl.seq_begin.push_back(S);
   return pl;
@@ -1756,10 +1756,17 @@ static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_
 }
 
 static int64_t slab_cap(const fastrl_loss_args& a) {
-  if (a.slab_tokens > 0) return a.slab_tokens;
-  const int64_t esz = a.dtype == FASTRL_BF16 ? 2 : 4;
-  const int64_t cap = kDefaultSlabBytes / (rup(a.V, kBM) * esz);
-  return std::max<int64_t>(4096, cap / kBN * kBN);
+  return a.slab_tokens > 0 ? a.slab_tokens : kDefaultSlabTokens;
+}
+
+int policy_loss_slab_plan(const fastrl_loss_args& a, int32_t* seq_begin, int32_t capacity,
+                          int64_t* tc_max) {
+  SlabPlan pl = plan_slabs(a.seq_off_host, a.S, slab_cap(a));
+  const int32_t n = int32_t(pl.seq_begin.size()) - 1;
+  if (tc_max) *tc_max = pl.tc_max;
+  if (seq_begin && capacity > n)
+    for (int32_t k = 0; k <= n; ++k) seq_begin[k] = pl.seq_begin[k];
+  return n;
 }
 
 size_t policy_loss_workspace(const fastrl_loss_args& a) {
@@ -1783,7 +1790,8 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
 
   hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, stream, w.redo_count, int64_t(1), 0);
   FR_LAUNCHED();
-  if (dw && !a.dW_accumulate && a.S == 0) {
+  // no token at all (S == 0, or only empty sequences): no GEMM writes dW
+  if (dw && !a.dW_accumulate && a.T == 0) {
     hipLaunchKernelGGL(fill_i32_kernel, dim3(1024), dim3(256), 0, stream,
                        reinterpret_cast<int32_t*>(a.dW), int64_t(V) * d, 0);
     FR_LAUNCHED();
@@ -1796,13 +1804,23 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
     FR_LAUNCHED();
   }
   const size_t nslab = pl.seq_begin.size() - 1;
+  bool dw_written = false;  // a slab's dW GEMM has overwritten dW
   for (size_t si = 0; si < nslab; ++si) {
     const int32_t s0 = pl.seq_begin[si], s1 = pl.seq_begin[si + 1];
     const int64_t t0 = a.seq_off_host[s0];
     const int32_t Tc = int32_t(a.seq_off_host[s1] - t0);
-    const int64_t Tr = rup(std::max<int32_t>(Tc, 1), kBN);
+    if (Tc == 0) {  // only empty sequences (T == 0): their loss terms and clip counts are 0
+      hipLaunchKernelGGL(loss_kernel, dim3(unsigned(s1 - s0)), dim3(256), 0, stream, w.logp,
+                         w.lse, a.old_logp, a.ref_logp, a.row_index, a.seq_off, a.adv,
+                         a.seq_index, a.S, a.T, s0, t0, a.algo, a.norm, a.eps_low, a.eps_high,
+                         a.beta, w.shift, w.gslab, w.cslab, w.seq_loss, w.seq_clip, a.status,
+                         a.seq_index ? INT32_MAX : a.S);
+      FR_LAUNCHED();
+      continue;
+    }
+    const int64_t Tr = rup(Tc, kBN);
     const int32_t nnb = int32_t(Tr / kBN);
-    hipLaunchKernelGGL(slab_prep_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0, stream,
+    hipLaunchKernelGGL(slab_prep_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream,
                        a.token_ids, a.row_index, t0, Tc, V, w.yslab, w.shift, a.status);
     FR_LAUNCHED();
     hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(256), 0, stream, w.redo_blk,
@@ -1819,7 +1837,7 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
     const double f_fwd = 2.0 * double(V) * Tc * d;
     FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, f_fwd, stream)));
     const bool store = dh || dw;
-    hipLaunchKernelGGL(merge_kernel, dim3(nb1d(std::max(Tc, 1), 64)), dim3(256), 0, stream,
+    hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 64)), dim3(256), 0, stream,
                        w.pmax, w.psum, w.psz, tcp, nmb, w.zlab, w.yslab, Tc, store ? 1 : 0,
                        store ? 1 : 0, w.lse + t0, w.logp + t0, w.ent ? w.ent + t0 : nullptr,
                        store ? w.shift : (float*)nullptr, w.redo_blk, w.redo_count);
@@ -1828,7 +1846,7 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
       // token blocks holding a row that needs a shift: evaluate again, then merge again
       p.store_e = 2;
       FR_TRY((launch_gemm<T, MODE_FWD>(p, -1, 0.0, stream)));
-      hipLaunchKernelGGL(merge_kernel, dim3(nb1d(std::max(Tc, 1), 64)), dim3(256), 0, stream,
+      hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 64)), dim3(256), 0, stream,
                          w.pmax, w.psum, w.psz, tcp, nmb, w.zlab, w.yslab, Tc, 1, 0, w.lse + t0,
                          w.logp + t0, w.ent ? w.ent + t0 : nullptr, w.shift, w.redo_blk,
                          w.redo_count);
@@ -1862,36 +1880,35 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
       hipLaunchKernelGGL(fill_i32_kernel, dim3(256), dim3(256), 0, stream, w.lab_cnt,
                          int64_t(V), 0);
       FR_LAUNCHED();
-      hipLaunchKernelGGL(label_hist_kernel, dim3(nb1d(std::max(Tc, 1), 256)), dim3(256), 0,
+      hipLaunchKernelGGL(label_hist_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0,
                          stream, w.yslab, Tc, w.lab_cnt);
       FR_LAUNCHED();
       hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, w.lab_cnt, V, w.lab_off);
       FR_LAUNCHED();
-      if (Tc > 0) {  // label CSR in (label, token) order: bitonic sort of the slab's keys
-        const int64_t n = sort_len(Tc);
-        hipLaunchKernelGGL(label_key_kernel, dim3(unsigned(n / 256)), dim3(256), 0, stream,
-                           w.yslab, Tc, n, w.lab_key);
-        FR_LAUNCHED();
-        hipLaunchKernelGGL(bitonic_tile_kernel, dim3(unsigned(n / kSortTile)), dim3(1024), 0,
-                           stream, w.lab_key, int64_t(0));
-        FR_LAUNCHED();
-        for (int64_t k = 2 * kSortTile; k <= n; k <<= 1) {
-          for (int64_t j = k / 2; j >= kSortTile; j >>= 1) {
-            hipLaunchKernelGGL(bitonic_step_kernel, dim3(unsigned(n / 2 / 256)), dim3(256), 0,
-                               stream, w.lab_key, n, k, j);
-            FR_LAUNCHED();
-          }
-          hipLaunchKernelGGL(bitonic_tile_kernel, dim3(unsigned(n / kSortTile)), dim3(1024), 0,
-                             stream, w.lab_key, k);
+      // label CSR in (label, token) order: bitonic sort of the slab's keys
+      const int64_t n = sort_len(Tc);
+      hipLaunchKernelGGL(label_key_kernel, dim3(unsigned(n / 256)), dim3(256), 0, stream,
+                         w.yslab, Tc, n, w.lab_key);
+      FR_LAUNCHED();
+      hipLaunchKernelGGL(bitonic_tile_kernel, dim3(unsigned(n / kSortTile)), dim3(1024), 0,
+                         stream, w.lab_key, int64_t(0));
+      FR_LAUNCHED();
+      for (int64_t k = 2 * kSortTile; k <= n; k <<= 1) {
+        for (int64_t j = k / 2; j >= kSortTile; j >>= 1) {
+          hipLaunchKernelGGL(bitonic_step_kernel, dim3(unsigned(n / 2 / 256)), dim3(256), 0,
+                             stream, w.lab_key, n, k, j);
           FR_LAUNCHED();
         }
-        hipLaunchKernelGGL(label_tok_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream,
-                           w.lab_key, Tc, w.lab_tok);
+        hipLaunchKernelGGL(bitonic_tile_kernel, dim3(unsigned(n / kSortTile)), dim3(1024), 0,
+                           stream, w.lab_key, k);
         FR_LAUNCHED();
       }
+      hipLaunchKernelGGL(label_tok_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream,
+                         w.lab_key, Tc, w.lab_tok);
+      FR_LAUNCHED();
       GemmParams q{};
       q.K = int32_t(Tr);
-      q.dW = a.dW; q.dW_acc = (si > 0 || a.dW_accumulate) ? 1 : 0;
+      q.dW = a.dW; q.dW_acc = (dw_written || a.dW_accumulate) ? 1 : 0;
       q.d = d;
       q.status = a.status;
       if constexpr (sizeof(T) == 2) {  // dW^T = Bd E: A = Bd, B = E1 read K-major
@@ -1903,16 +1920,15 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
         q.B = w.Bd; q.ldb = tcp; q.N = d;
         FR_TRY((launch_gemm<T, MODE_DW>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
       }
-      if (Tc > 0) {
-        const unsigned nch = unsigned((Tc + kOneHotChunk - 1) / kOneHotChunk);
-        hipLaunchKernelGGL((dw_onehot_kernel<T>), dim3(nch), dim3(256), 0, stream, w.lab_off,
-                           w.lab_tok, w.yslab, w.gslab, static_cast<const T*>(a.hidden),
-                           a.row_index, t0, d, V, a.dW, w.oh_head, w.oh_tail);
-        FR_LAUNCHED();
-        hipLaunchKernelGGL(dw_onehot_carry_kernel, dim3(nch), dim3(256), 0, stream, w.lab_off,
-                           w.lab_tok, w.yslab, d, V, a.dW, w.oh_head, w.oh_tail);
-        FR_LAUNCHED();
-      }
+      dw_written = true;
+      const unsigned nch = unsigned((Tc + kOneHotChunk - 1) / kOneHotChunk);
+      hipLaunchKernelGGL((dw_onehot_kernel<T>), dim3(nch), dim3(256), 0, stream, w.lab_off,
+                         w.lab_tok, w.yslab, w.gslab, static_cast<const T*>(a.hidden),
+                         a.row_index, t0, d, V, a.dW, w.oh_head, w.oh_tail);
+      FR_LAUNCHED();
+      hipLaunchKernelGGL(dw_onehot_carry_kernel, dim3(nch), dim3(256), 0, stream, w.lab_off,
+                         w.lab_tok, w.yslab, d, V, a.dW, w.oh_head, w.oh_tail);
+      FR_LAUNCHED();
     }
   }
   hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, stream, w.seq_loss, w.seq_clip,
