@@ -15,7 +15,10 @@ its launch stream during the timed steps; ``cpu_baseline`` times the fp64 oracle
 bounded sample of the same workload.  ``rows`` (after the timed steps, skipped with
 --no-rows) times the parts beyond the step on the same workload: pruning with
 continuous-reward groups, the DP-alignment fill, the entropy accumulator (one loss call with
-and without it) and the AdamW update of W (bytes per second against HBM).
+and without it), the forward-only log-prob pass of the old and ref policies, and the AdamW
+update of W (bytes per second against HBM).  Every call of the warmup and timed steps
+reports into one device status word; any bit other than the informational SHIFT_REDO makes
+the run exit with status 3 and no result line.
 
 usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 3] [--no-cpu]
                        [--no-rows]
@@ -33,6 +36,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 MFMA
+SHIFT_REDO = 0x40           # informational status bit (rows re-evaluated with a shift)
+DEFAULT_SLAB = 32768        # the library's slab when slab_tokens is 0
 
 
 def parse():
@@ -44,6 +49,8 @@ def parse():
     ap.add_argument("--slab", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=768)
+    ap.add_argument("--cpu-tokens-1t", type=int, default=16,
+                    help="tokens of the one-thread oracle sample (0: skip it)")
     ap.add_argument("--no-rows", action="store_true",
                     help="skip the timings of the additional rows")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -109,7 +116,7 @@ def make_inputs(cfg, dev, fr):
     return ro, inp
 
 
-def cpu_baseline(cfg, ro, inp, n_tokens):
+def cpu_baseline(cfg, ro, inp, n_tokens, n_tokens_1t=0):
     """The oracle, as it stands, on a bounded sample: advantage + pruning + compaction of
     the whole batch, then the LM-head forward, loss and full backward (dH and dW at full
     V x d) for the first kept sequences holding >= n_tokens tokens."""
@@ -134,29 +141,49 @@ def cpu_baseline(cfg, ro, inp, n_tokens):
     Wd = inp["W"].float().cpu().numpy().astype(np.float64)
     old = inp["old"].cpu().numpy()
     ref = inp["ref"].cpu().numpy() if inp["ref"] is not None else None
-    t0 = time.perf_counter()
-    pr = oracle.hot_path_step(ro.rewards, ro.group_off, ro.token_ids, ro.traj_tok_off,
-                              lmhead=False, keep_ratio=cfg.keep_ratio,
-                              drop_uniform=cfg.drop_uniform)
-    koff = pr["kept_tok_off"]
-    S = int(np.searchsorted(koff, n_tokens)) if koff[-1] >= n_tokens else len(koff) - 1
-    S = max(1, min(S, len(koff) - 1))
-    src = pr["tok_src"][:koff[S]]
-    Hk = H[torch_index(src, H.device)].float().cpu().numpy().astype(np.float64)
-    y = ro.token_ids[src].astype(np.int64)
-    logp, lse = oracle.token_logprob(Hk, Wd, y)
-    loss, g, _ = oracle.policy_loss(logp, old[src].astype(np.float64),
-                                    None if ref is None else ref[src].astype(np.float64),
-                                    koff[:S + 1], pr["adv"][pr["kept_traj"][:S]],
-                                    algo=cfg.algo, norm=cfg.norm, eps_low=cfg.eps_low,
-                                    eps_high=cfg.eps_high, beta=cfg.beta)
-    dH, dW = oracle.lmhead_backward(Hk, Wd, y, lse, g)
-    dt = time.perf_counter() - t0
-    return dict(value=len(src) / dt, unit="kept tokens/s", cores=int(cores), kind="oracle",
-                cpu=cpu, blas=blas,
-                sample=f"whole batch advantage+MDAP+compaction, then LM-head fwd + loss + "
-                       f"full bwd (dH, dW at V={cfg.V}, d={cfg.d}) in fp64 for the first "
-                       f"{S} kept sequences ({len(src)} tokens); {dt:.1f} s")
+
+    def run(tokens, cut=False):
+        """Whole kept sequences holding >= tokens tokens; with cut, exactly the first
+        tokens kept tokens (the last sequence truncated)."""
+        t0 = time.perf_counter()
+        pr = oracle.hot_path_step(ro.rewards, ro.group_off, ro.token_ids, ro.traj_tok_off,
+                                  lmhead=False, keep_ratio=cfg.keep_ratio,
+                                  drop_uniform=cfg.drop_uniform)
+        koff = pr["kept_tok_off"]
+        S = int(np.searchsorted(koff, tokens)) if koff[-1] >= tokens else len(koff) - 1
+        S = max(1, min(S, len(koff) - 1))
+        if cut:
+            koff = np.minimum(koff, tokens)
+        src = pr["tok_src"][:koff[S]]
+        Hk = H[torch_index(src, H.device)].float().cpu().numpy().astype(np.float64)
+        y = ro.token_ids[src].astype(np.int64)
+        logp, lse = oracle.token_logprob(Hk, Wd, y)
+        loss, g, _ = oracle.policy_loss(logp, old[src].astype(np.float64),
+                                        None if ref is None else ref[src].astype(np.float64),
+                                        koff[:S + 1], pr["adv"][pr["kept_traj"][:S]],
+                                        algo=cfg.algo, norm=cfg.norm, eps_low=cfg.eps_low,
+                                        eps_high=cfg.eps_high, beta=cfg.beta)
+        oracle.lmhead_backward(Hk, Wd, y, lse, g)
+        return S, len(src), time.perf_counter() - t0
+
+    S, n, dt = run(n_tokens)
+    res = dict(value=n / dt, unit="kept tokens/s", cores=int(cores), kind="oracle",
+               cpu=cpu, blas=blas,
+               sample=f"whole batch advantage+MDAP+compaction, then LM-head fwd + loss + "
+                      f"full bwd (dH, dW at V={cfg.V}, d={cfg.d}) in fp64 for the first "
+                      f"{S} kept sequences ({n} tokens); {dt:.1f} s")
+    if n_tokens_1t > 0:
+        try:
+            from threadpoolctl import threadpool_limits
+            with threadpool_limits(limits=1):
+                S1, n1, dt1 = run(n_tokens_1t, cut=True)
+            res["one_thread"] = dict(value=n1 / dt1, unit="kept tokens/s", cores=1,
+                                     sample=f"the same for the first {n1} kept tokens "
+                                            f"({S1} sequences, the last one cut) with one "
+                                            f"BLAS thread; {dt1:.1f} s")
+        except ImportError:
+            res["one_thread"] = None
+    return res
 
 
 def _time_gpu(fn, reps):
@@ -207,7 +234,6 @@ def extra_rows(cfg, ro, inp, fr, max_group, max_len, last, args):
     # without the extra accumulator
     call = last["call"]
     koff = last["kept_tok_off_host"]
-    pr = last["prune"]
     mk = lambda ent: fr.LossCall(inp["H"], inp["W"], inp["token_ids"], inp["old"],
                                  pr["kept_tok_off"], koff, last["adv"], ref_logp=inp["ref"],
                                  seq_index=pr["kept_traj"], row_index=pr["tok_src"],
@@ -227,6 +253,20 @@ def extra_rows(cfg, ro, inp, fr, max_group, max_len, last, args):
     rows["entropy_in_lse_pass"] = dict(ms_loss_call=ent_ms, ms_loss_call_without=base_ms,
                                        overhead=ent_ms / base_ms - 1.0,
                                        mean_entropy=mean_ent)
+    # the old and ref passes of the step (Table timing_breakdown's timing_old / timing_ref):
+    # forward-only log-probs of the kept tokens, no exp-logit slab
+    pr = last["prune"]
+    tk = last["t_kept"]
+    src = pr["tok_src"]
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    lp_ms = _time_gpu(lambda: fr.token_logprob(inp["H"], inp["W"], inp["token_ids"],
+                                               row_index=src, T=tk, status=st), 5)
+    assert int(st.item()) == 0, fr.status_names(int(st.item()))
+    lp_tf = 2.0 * cfg.V * cfg.d * tk / (lp_ms * 1e-3) / 1e12
+    rows["token_logprob_old_ref_pass"] = dict(
+        ms=lp_ms, kept_tokens=tk, kept_tokens_per_s=tk / (lp_ms * 1e-3), tflops=lp_tf,
+        frac_of_peak=lp_tf / PEAK_BF16_TFLOPS,
+        note="fastrl_token_logprob over the kept tokens (2 V d FLOP per token)")
     # N3: AdamW on W (float32 master, moments, dW; bf16 copy): 30 bytes per parameter
     n = cfg.V * cfg.d
     th = inp["W"].float().reshape(-1).contiguous()
@@ -270,6 +310,10 @@ def main():
     max_group = int(np.diff(ro.group_off).max())
     max_len = int(ro.lengths.max())
 
+    # device status word of every call in the warmup and timed steps: read once after the
+    # timed loop; a data fault or a timed-out stage hand-over invalidates the line
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+
     def step():
         return fr.hot_path_step(
             inp["rewards"], inp["group_off"], inp["token_ids"], inp["traj_tok_off"],
@@ -277,7 +321,7 @@ def main():
             max_len=max_len, algo=cfg.algo, norm=cfg.norm, eps_low=cfg.eps_low,
             eps_high=cfg.eps_high, beta=cfg.beta, ngram_n=cfg.ngram_n,
             tau=(cfg.tau_num, cfg.tau_den), keep_ratio=cfg.keep_ratio,
-            drop_uniform=cfg.drop_uniform, slab_tokens=args.slab)
+            drop_uniform=cfg.drop_uniform, slab_tokens=args.slab, status=status)
 
     for i in range(args.warmup):
         out = step()
@@ -303,6 +347,13 @@ def main():
     elapsed = time.perf_counter() - t0
     fr.profile_enable(False)
     log(f"[bench] {args.steps} timed steps in {elapsed:.3f} s")
+    word = int(status.item())
+    fatal = word & ~SHIFT_REDO
+    if fatal:
+        log(f"[bench] INVALID: device status {word:#x} {fr.status_names(word)} after the "
+            "warmup and timed steps; no result line")
+        sys.exit(3)
+    slab_begin, slab_max = out["call"].slab_plan()
     kinds = {fr.K_LOGITS_FWD: "logits_fwd", fr.K_DHIDDEN: "dhidden", fr.K_DW: "dW"}
     per = {}
     for k, name in kinds.items():
@@ -333,7 +384,10 @@ def main():
                                f"U[{cfg.len_lo},{cfg.len_hi}], d={cfg.d}, V={cfg.V}, "
                                f"keep ratio {cfg.keep_ratio}, beta {cfg.beta}",
                    "kept_tokens_per_step": t_kept, "kept_sequences": out["n_kept"],
-                   "total_tokens": ro.T_total, "parallelism": "single GPU"},
+                   "total_tokens": ro.T_total, "parallelism": "single GPU",
+                   "slab_tokens": args.slab or DEFAULT_SLAB, "slabs": len(slab_begin) - 1,
+                   "max_slab_tokens": slab_max},
+        "status_word": word,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": ach, "peak": peak,
                      "unit": "TFLOP/s", "frac": ach / peak,
                      "traffic": measured_traffic(dom) if cfg.name == CONFIGS[3].name else None},
@@ -346,7 +400,7 @@ def main():
         res["rows"] = extra_rows(cfg, ro, inp, fr, max_group, max_len, out, args)
     if not args.no_cpu:
         log("[bench] timing the oracle on a CPU sample")
-        res["cpu_baseline"] = cpu_baseline(cfg, ro, inp, args.cpu_tokens)
+        res["cpu_baseline"] = cpu_baseline(cfg, ro, inp, args.cpu_tokens, args.cpu_tokens_1t)
     print(json.dumps(res), flush=True)
 
 

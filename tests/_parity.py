@@ -1,7 +1,8 @@
 """Shared helpers of the GPU parity tests: build one seeded problem, run the oracle and
 the HIP path (through the C ABI) on the same inputs, compare with the stated bars:
 pruning masks / indices bit-exact, log-probs 2e-3 absolute, loss and gradients 1e-2
-relative (bf16 inputs, fp32 accumulate)."""
+relative (bf16 inputs, fp32 accumulate): for gradients both the whole-matrix relative
+Frobenius error and the largest per-row relative error."""
 import dataclasses
 
 import numpy as np
@@ -116,18 +117,32 @@ def onehot_parts(H, W, y, g):
     return dH1, dW1
 
 
+def row_rel(a, b):
+    """Largest per-row relative error max_r ||a_r - b_r|| / ||b_r|| (rows whose reference is
+    exactly zero must be exactly zero: they count as 0 or inf)."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    num = np.linalg.norm(a - b, axis=1)
+    den = np.linalg.norm(b, axis=1)
+    r = np.where(den > 0, num / np.where(den > 0, den, 1.0), np.where(num > 0, np.inf, 0.0))
+    return float(r.max()) if len(r) else 0.0
+
+
 def check_grads(H, W, y, g_ref, dH_gpu, dW_gpu, dH_ref, dW_ref, rel=REL):
-    """Whole-gradient relative Frobenius error, and the same for the softmax part alone
-    (the dense GEMM part; the one-hot part dominates the norm)."""
+    """Whole-gradient relative Frobenius error, the same for the softmax part alone (the
+    dense GEMM part; the one-hot part dominates the norm), and the largest per-row relative
+    error (every token's dhidden row, every vocabulary row of dW)."""
     out = {}
     if dH_gpu is not None:
         out["dH"] = rel_fro(dH_gpu, dH_ref)
         dH1, _ = onehot_parts(H, W, y, g_ref)
         out["dH_soft"] = rel_fro(dH_gpu - dH1, dH_ref - dH1)
+        out["dH_row"] = row_rel(dH_gpu, dH_ref)
     if dW_gpu is not None:
         out["dW"] = rel_fro(dW_gpu, dW_ref)
         _, dW1 = onehot_parts(H, W, y, g_ref)
         out["dW_soft"] = rel_fro(dW_gpu - dW1, dW_ref - dW1)
+        out["dW_row"] = row_rel(dW_gpu, dW_ref)
     for k, v in out.items():
         assert v <= rel, (k, v, out)
     return out

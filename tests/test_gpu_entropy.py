@@ -70,4 +70,6 @@ def test_entropy_on_the_shifted_path(fr):
     assert call.stats[1].item() > 0
     T = len(pb.src)
     got = call.entropy[:T].double().cpu().numpy()
-    assert np.abs(got - want).max() < LOGP_ATOL * 50
+    err = np.abs(got - want).max()
+    print(f"shifted-path entropy max error {err:.3e}")
+    assert err < ENT_ATOL, err
