@@ -220,6 +220,27 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
                          int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------------------
+ * fastrl_token_logprob_noalloc -- fastrl_token_logprob for callers that cannot allocate
+ * device memory or pass a workspace (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): same arguments, results and errors (results are bit
+ * for bit those of fastrl_token_logprob), without ws / ws_bytes.  It calls no allocating
+ * routine; its scratch is a fixed device array of fastrl_token_logprob_noalloc_scratch_bytes()
+ * (64 MiB) that every GPU the library runs on holds from its first use until the process
+ * ends.  The tokens run in chunks of fastrl_token_logprob_noalloc_max_chunk(V) (14080 at
+ * V = 152064); a V for which not even 256 tokens fit gives FASTRL_ERR_SHAPE (V above ~8.38M).
+ * `stream` must belong to the current device (FASTRL_ERR_VALUE otherwise).  All calls on one
+ * GPU share its array: calls that overlap on one GPU (other streams, other threads) race and
+ * must be serialised by the caller.  The first call on a device looks the array's address
+ * up (hipGetSymbolAddress) with that device current.
+ * ------------------------------------------------------------------------------------ */
+int fastrl_token_logprob_noalloc(const void* hidden, const int32_t* row_index, const void* W,
+                                 int32_t dtype, int64_t T, int32_t d, int32_t V,
+                                 const int32_t* token_ids, float* logp, float* lse,
+                                 int32_t* status, hipStream_t stream);
+size_t fastrl_token_logprob_noalloc_scratch_bytes(void);
+int64_t fastrl_token_logprob_noalloc_max_chunk(int32_t V);
+
+/* ------------------------------------------------------------------------------------
  * fastrl_policy_loss_fwd_bwd -- Sec. 3.1: the clipped surrogate of Eq. (1) (loss = -J),
  * its per-token coefficient g_t = dL/dlogp_t (Eq. grad; clipping indicator with inclusive
  * edges), and the LM-head backward dZ = g (onehot(y) - softmax(z)), dhidden = dZ W,

@@ -86,6 +86,10 @@ _SIGS = {
     "fastrl_token_logprob_workspace_size": (_sz, [_i64, _i32, _i32, _i32]),
     "fastrl_token_logprob": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i64, _i32, _i32, _vp, _vp,
                                             _vp, _vp, _vp, _sz, _vp]),
+    "fastrl_token_logprob_noalloc": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i64, _i32, _i32,
+                                                    _vp, _vp, _vp, _vp, _vp]),
+    "fastrl_token_logprob_noalloc_scratch_bytes": (_sz, []),
+    "fastrl_token_logprob_noalloc_max_chunk": (_i64, [_i32]),
     "fastrl_loss_args_size": (_sz, []),
     "fastrl_policy_loss_workspace_size": (_sz, [ctypes.POINTER(LossArgs)]),
     "fastrl_policy_loss_fwd_bwd": (ctypes.c_int, [ctypes.POINTER(LossArgs), _vp]),
@@ -260,6 +264,31 @@ def token_logprob(hidden, W, token_ids, row_index=None, T=None, status=None):
                                      _p(token_ids), _p(logp), _p(lse), _p(status), _p(ws),
                                      ws.numel(), _stream()), "fastrl_token_logprob")
     return logp[:T], lse[:T]
+
+
+def token_logprob_noalloc(hidden, W, token_ids, logp, lse=None, row_index=None, T=None,
+                          status=None):
+    """fastrl_token_logprob_noalloc: the same log-probs with the library's fixed scratch
+    and no workspace; the caller passes the outputs (logp, and lse or None), so nothing is
+    allocated on this path."""
+    _dev(hidden)
+    dt = _dtype_code(hidden)
+    d = hidden.shape[1]
+    V = W.shape[0]
+    for t, dty, nm in ((hidden, hidden.dtype, "hidden"), (W, hidden.dtype, "W"),
+                       (token_ids, torch.int32, "token_ids"), (row_index, torch.int32,
+                       "row_index"), (status, torch.int32, "status"),
+                       (logp, torch.float32, "logp"), (lse, torch.float32, "lse")):
+        _arg(t, dty, nm)
+    if W.shape[1] != d:
+        raise FastRLError("W must be [V, d] with the hidden size of `hidden`")
+    if T is None:
+        T = row_index.numel() if row_index is not None else hidden.shape[0]
+    if logp.numel() < T or (lse is not None and lse.numel() < T):
+        raise FastRLError("logp / lse must hold T entries")
+    _check(_lib.fastrl_token_logprob_noalloc(_p(hidden), _p(row_index), _p(W), dt, T, d, V,
+                                             _p(token_ids), _p(logp), _p(lse), _p(status),
+                                             _stream()), "fastrl_token_logprob_noalloc")
 
 
 class LossCall:

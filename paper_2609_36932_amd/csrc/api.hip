@@ -20,6 +20,11 @@ int launch_prune(const int32_t*, const int64_t*, int64_t, const float*, const in
                  int32_t*, int32_t*, int32_t, int32_t*, int64_t*, int32_t*, int64_t*, int32_t*,
                  void*, hipStream_t);
 size_t token_logprob_workspace(int64_t T, int32_t d, int32_t V, int32_t dtype);
+int run_token_logprob_noalloc(const void*, const int32_t*, const void*, int32_t, int64_t,
+                              int32_t, int32_t, const int32_t*, float*, float*, int32_t*,
+                              hipStream_t);
+size_t token_logprob_noalloc_scratch_bytes();
+int64_t token_logprob_noalloc_chunk(int32_t V);
 int run_token_logprob(const void*, const int32_t*, const void*, int32_t, int64_t, int32_t,
                       int32_t, const int32_t*, float*, float*, int32_t*, void*, hipStream_t);
 size_t policy_loss_workspace(const fastrl_loss_args& a);
@@ -211,6 +216,35 @@ int fastrl_token_logprob(const void* hidden, const int32_t* row_index, const voi
                    std::to_string(need) + " bytes");
   return run_token_logprob(hidden, row_index, W, dtype, T, d, V, token_ids, logp, lse, status,
                            ws, stream);
+}
+
+int fastrl_token_logprob_noalloc(const void* hidden, const int32_t* row_index, const void* W,
+                                 int32_t dtype, int64_t T, int32_t d, int32_t V,
+                                 const int32_t* token_ids, float* logp, float* lse,
+                                 int32_t* status, hipStream_t stream) {
+  clear_error();
+  FR_CHECK_ARG(dtype == FASTRL_F32 || dtype == FASTRL_BF16, FASTRL_ERR_DTYPE,
+               "fastrl_token_logprob_noalloc: dtype must be FASTRL_F32 or FASTRL_BF16");
+  FR_CHECK_ARG(T >= 0 && d >= 8 && d % 8 == 0 && V >= 1, FASTRL_ERR_SHAPE,
+               "fastrl_token_logprob_noalloc: need T >= 0, d a positive multiple of 8, V >= 1");
+  FR_CHECK_ARG(T < (int64_t(1) << 31) && V < (1 << 30), FASTRL_ERR_SHAPE,
+               "fastrl_token_logprob_noalloc: T or V too large");
+  if (T > 0) {
+    FR_CHECK_ARG(hidden && W && token_ids && logp, FASTRL_ERR_NULL_PTR,
+                 "fastrl_token_logprob_noalloc: hidden / W / token_ids / logp is NULL");
+    FR_CHECK_ARG(aligned16(hidden) && aligned16(W), FASTRL_ERR_VALUE,
+                 "fastrl_token_logprob_noalloc: hidden and W must be 16-byte aligned");
+  }
+  return run_token_logprob_noalloc(hidden, row_index, W, dtype, T, d, V, token_ids, logp, lse,
+                                   status, stream);
+}
+
+size_t fastrl_token_logprob_noalloc_scratch_bytes(void) {
+  return token_logprob_noalloc_scratch_bytes();
+}
+
+int64_t fastrl_token_logprob_noalloc_max_chunk(int32_t V) {
+  return V >= 1 ? token_logprob_noalloc_chunk(V) : 0;
 }
 
 static int check_loss_args(const fastrl_loss_args* a, bool need_ws) {

@@ -27,6 +27,8 @@
 // default slab (32768 tokens) does not grow with T.
 #include <algorithm>
 #include <cstdlib>
+#include <mutex>
+#include <string>
 #include <vector>
 
 #include "common.h"
@@ -1601,8 +1603,12 @@ struct LogprobWs {
   int32_t* yslab;
 };
 
-static size_t carve_logprob(Carver& c, LogprobWs& w, int64_t T, int32_t V) {
-  const int64_t ch = rup(std::min<int64_t>(std::max<int64_t>(T, 1), kLogprobChunk), 256);
+// tokens per chunk for T tokens when at most `chunk` fit (a multiple of 256)
+static int64_t logprob_chunk(int64_t T, int64_t chunk) {
+  return rup(std::min<int64_t>(std::max<int64_t>(T, 1), chunk), 256);
+}
+
+static size_t carve_logprob(Carver& c, LogprobWs& w, int64_t ch, int32_t V) {
   const int64_t nmb = (V + kBM - 1) / kBM;
   w.pmax = c.take<float>(size_t(nmb * ch));
   w.psum = c.take<float>(size_t(nmb * ch));
@@ -1616,20 +1622,23 @@ size_t token_logprob_workspace(int64_t T, int32_t d, int32_t V, int32_t dtype) {
   (void)dtype;
   Carver c(nullptr);
   LogprobWs w;
-  return carve_logprob(c, w, T, V);
+  return carve_logprob(c, w, logprob_chunk(T, kLogprobChunk), V);
 }
 
+// Chunks of at most `chunk` tokens through the logits GEMM (partials only) and the merge;
+// every token's result depends on its own logits alone, so the chunking changes nothing.
+// prof: record the GEMM launches in the kernel-timing recorder.
 template <typename T>
 static int token_logprob_impl(const void* hidden, const int32_t* row_index, const void* W,
                               int64_t Tn, int32_t d, int32_t V, const int32_t* token_ids,
                               float* logp, float* lse, int32_t* status, void* ws,
-                              hipStream_t stream) {
+                              int64_t chunk, bool prof, hipStream_t stream) {
   Carver c(ws);
   LogprobWs w;
-  carve_logprob(c, w, Tn, V);
-  const int64_t ch = rup(std::min<int64_t>(std::max<int64_t>(Tn, 1), kLogprobChunk), 256);
-  for (int64_t t0 = 0; t0 < Tn; t0 += kLogprobChunk) {
-    const int32_t Tc = int32_t(std::min<int64_t>(kLogprobChunk, Tn - t0));
+  const int64_t ch = logprob_chunk(Tn, chunk);
+  carve_logprob(c, w, ch, V);
+  for (int64_t t0 = 0; t0 < Tn; t0 += ch) {
+    const int32_t Tc = int32_t(std::min<int64_t>(ch, Tn - t0));
     hipLaunchKernelGGL(slab_prep_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream, token_ids,
                        row_index, t0, Tc, V, w.yslab, (float*)nullptr, status);
     FR_LAUNCHED();
@@ -1639,7 +1648,8 @@ static int token_logprob_impl(const void* hidden, const int32_t* row_index, cons
     p.K = d;
     p.pmax = w.pmax; p.psum = w.psum; p.ldp = ch; p.zlab = w.zlab; p.yslab = w.yslab;
     p.Vreal = V; p.store_e = 0; p.status = status;
-    FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, 2.0 * V * double(Tc) * d, stream)));
+    FR_TRY((launch_gemm<T, MODE_FWD>(p, prof ? FASTRL_K_LOGITS_FWD : -1,
+                                     2.0 * V * double(Tc) * d, stream)));
     const int32_t nmb = (V + kBM - 1) / kBM;
     hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 64)), dim3(256), 0, stream, w.pmax, w.psum,
                        (const float*)nullptr, ch, nmb, w.zlab, w.yslab, Tc, 0, 0,
@@ -1656,9 +1666,78 @@ int run_token_logprob(const void* hidden, const int32_t* row_index, const void* 
                       void* ws, hipStream_t stream) {
   if (dtype == FASTRL_BF16)
     return token_logprob_impl<uint16_t>(hidden, row_index, W, T, d, V, token_ids, logp, lse,
-                                        status, ws, stream);
+                                        status, ws, kLogprobChunk, true, stream);
   return token_logprob_impl<float>(hidden, row_index, W, T, d, V, token_ids, logp, lse, status,
-                                   ws, stream);
+                                   ws, kLogprobChunk, true, stream);
+}
+
+// ---- the allocation-free variant: its scratch is a fixed device array --------------------
+// kNoAllocScratchBytes of device memory per GPU, held from the library's first use on that
+// GPU until the process ends.  In host code `scratch` names a host-side stand-in, not the
+// device copy: its device address is fetched once per device (hipGetSymbolAddress, with that
+// device current) and only that address reaches kernels.  Every call on a GPU shares that
+// GPU's array, so calls that overlap on one GPU (two streams, two threads) race.  Nothing in
+// it has to start at zero: each chunk writes every partial, label and logit it reads.
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_dev[kMaxScratchDevices] = {};
+
+size_t token_logprob_noalloc_scratch_bytes() { return kNoAllocScratchBytes; }
+
+// the most tokens per chunk (a multiple of 256) whose partials fit in the scratch; 0 if not
+// even 256 do
+int64_t token_logprob_noalloc_chunk(int32_t V) {
+  int64_t lo = 0;
+  for (int64_t ch = 256; ch <= kLogprobChunk; ch += 256) {
+    Carver c(nullptr);
+    LogprobWs w;
+    if (carve_logprob(c, w, ch, V) > kNoAllocScratchBytes) break;
+    lo = ch;
+  }
+  return lo;
+}
+
+int run_token_logprob_noalloc(const void* hidden, const int32_t* row_index, const void* W,
+                              int32_t dtype, int64_t T, int32_t d, int32_t V,
+                              const int32_t* token_ids, float* logp, float* lse,
+                              int32_t* status, hipStream_t stream) {
+  const int64_t chunk = token_logprob_noalloc_chunk(V);
+  FR_CHECK_ARG(chunk >= 256, FASTRL_ERR_SHAPE,
+               "fastrl_token_logprob_noalloc: V = " + std::to_string(V) +
+                   " needs more than the fixed scratch of " +
+                   std::to_string(kNoAllocScratchBytes >> 20) + " MiB for 256 tokens");
+  int dev = -1;
+  FR_HIP(hipGetDevice(&dev));
+  FR_CHECK_ARG(dev >= 0 && dev < kMaxScratchDevices, FASTRL_ERR_UNSUPPORTED,
+               "fastrl_token_logprob_noalloc: device ordinal out of range");
+  if (stream) {
+    int sdev = -1;
+    FR_HIP(hipStreamGetDevice(stream, &sdev));
+    FR_CHECK_ARG(sdev == dev, FASTRL_ERR_VALUE,
+                 "fastrl_token_logprob_noalloc: the stream belongs to another device than the "
+                 "current one");
+  }
+  void* ptr = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+      void* p = nullptr;
+      FR_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+      FR_CHECK_ARG(p != nullptr, FASTRL_ERR_HIP,
+                   "fastrl_token_logprob_noalloc: no device address for the scratch array");
+      g_scratch_dev[dev] = p;
+    }
+    ptr = g_scratch_dev[dev];
+  }
+  if (T == 0) return FASTRL_OK;
+  if (dtype == FASTRL_BF16)
+    return token_logprob_impl<uint16_t>(hidden, row_index, W, T, d, V, token_ids, logp, lse,
+                                        status, ptr, chunk, false, stream);
+  return token_logprob_impl<float>(hidden, row_index, W, T, d, V, token_ids, logp, lse, status,
+                                   ptr, chunk, false, stream);
 }
 
 // ---------------------------------------------------------------- loss forward/backward
