@@ -234,6 +234,7 @@ def extra_rows(cfg, ro, inp, fr, max_group, max_len, last, args):
     # without the extra accumulator
     call = last["call"]
     koff = last["kept_tok_off_host"]
+    pr = last["prune"]
     mk = lambda ent: fr.LossCall(inp["H"], inp["W"], inp["token_ids"], inp["old"],
                                  pr["kept_tok_off"], koff, last["adv"], ref_logp=inp["ref"],
                                  seq_index=pr["kept_traj"], row_index=pr["tok_src"],
@@ -255,7 +256,6 @@ def extra_rows(cfg, ro, inp, fr, max_group, max_len, last, args):
                                        mean_entropy=mean_ent)
     # the old and ref passes of the step (Table timing_breakdown's timing_old / timing_ref):
     # forward-only log-probs of the kept tokens, no exp-logit slab
-    pr = last["prune"]
     tk = last["t_kept"]
     src = pr["tok_src"]
     st = torch.zeros(1, dtype=torch.int32, device=dev)
