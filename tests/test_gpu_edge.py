@@ -124,7 +124,8 @@ def test_zero_length_trajectories(fr, case):
     assert abs(call.loss.item() - ref["loss"]) <= REL * max(abs(ref["loss"]), 1e-12)
     assert int(call.stats[0].item()) == ref["clipped"]
     check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
-                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"])
+                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"],
+                dg=ref["dg"], lse=pb.lse_exact)
 
 
 @pytest.mark.parametrize("accumulate", [False, True])

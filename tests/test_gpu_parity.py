@@ -169,7 +169,8 @@ def test_hot_path_small(fr, case, slab):
     assert int(call.stats[0].item()) == ref["clipped"]
     Hk = pb.H64[pb.src]
     errs = check_grads(Hk, pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
-                       call.dW.double().cpu().numpy(), ref["dH"], ref["dW"])
+                       call.dW.double().cpu().numpy(), ref["dH"], ref["dW"],
+                dg=ref["dg"], lse=pb.lse_exact)
     print(case, slab, errs)
 
 
@@ -186,7 +187,8 @@ def test_cfg1_full(fr):
     assert np.abs(call.logp[:T].double().cpu().numpy() - pb.logp_exact).max() < 1e-4
     assert abs(call.loss.item() - ref["loss"]) <= 1e-4 * abs(ref["loss"])
     check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
-                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"], rel=1e-4)
+                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"], rel=1e-4, dg=pb.g_dev(1e-6),
+                lse=pb.lse_exact)
 
 
 def test_large_logits_take_the_shifted_path(fr):
@@ -205,7 +207,8 @@ def test_large_logits_take_the_shifted_path(fr):
     print(f"shifted-path logp max error {err:.3e}, lse {err_lse:.3e}")
     assert err < LOGP_ATOL and err_lse < LOGP_ATOL, (err, err_lse)
     check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
-                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"])
+                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"],
+                dg=ref["dg"], lse=pb.lse_exact)
 
 
 def test_deterministic(fr):
@@ -240,7 +243,8 @@ def test_head_heavy_labels(fr, skew, slab):
     assert T == len(pb.src) and int((pb.y == 0).sum()) > 2000
     call = a["call"]
     check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
-                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"])
+                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"],
+                dg=ref["dg"], lse=pb.lse_exact)
     assert torch.equal(call.dW, b["call"].dW)
 
 
