@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--slab", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=768)
+    ap.add_argument("--cpu-tokens", type=int, default=3072)
     ap.add_argument("--cpu-tokens-1t", type=int, default=16,
                     help="tokens of the one-thread oracle sample (0: skip it)")
     ap.add_argument("--no-rows", action="store_true",
