@@ -354,7 +354,8 @@ def main():
             "warmup and timed steps; no result line")
         sys.exit(3)
     slab_begin, slab_max = out["call"].slab_plan()
-    kinds = {fr.K_LOGITS_FWD: "logits_fwd", fr.K_DHIDDEN: "dhidden", fr.K_DW: "dW"}
+    kinds = {fr.K_LOGITS_FWD: "logits_fwd", fr.K_DHIDDEN: "dhidden", fr.K_DW: "dW",
+             fr.K_BACKWARD: "backward"}
     per = {}
     for k, name in kinds.items():
         ms, n, fl = fr.profile_read(k)

@@ -396,7 +396,9 @@ typedef enum fastrl_kernel_kind {
   FASTRL_K_LOGITS_FWD = 0,  /* logits GEMM + online log-sum-exp epilogue        */
   FASTRL_K_DHIDDEN = 1,     /* dhidden = dZ W GEMM                               */
   FASTRL_K_DW = 2,          /* dW = dZ^T hidden GEMM                             */
-  FASTRL_K_COUNT = 3
+  FASTRL_K_BACKWARD = 3,    /* dhidden and dW GEMMs of one slab in one launch
+                               (bf16 with both gradients asked for)              */
+  FASTRL_K_COUNT = 4
 } fastrl_kernel_kind;
 
 int fastrl_profile_enable(int32_t on);

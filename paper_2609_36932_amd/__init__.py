@@ -27,7 +27,7 @@ GRPO, DAPO, GSPO = 0, 1, 2
 NORM_SEQ_MEAN_TOKEN_MEAN, NORM_TOKEN_MEAN = 0, 1
 ALGOS = {"grpo": GRPO, "dapo": DAPO, "gspo": GSPO}
 NORMS = {"seq_mean_token_mean": NORM_SEQ_MEAN_TOKEN_MEAN, "token_mean": NORM_TOKEN_MEAN}
-K_LOGITS_FWD, K_DHIDDEN, K_DW = 0, 1, 2
+K_LOGITS_FWD, K_DHIDDEN, K_DW, K_BACKWARD = 0, 1, 2, 3
 STATUS_BITS = {0x1: "BAD_OFFSETS", 0x2: "BAD_TOKEN", 0x4: "GROUP_TOO_BIG",
                0x8: "SEQ_TOO_LONG", 0x10: "BAD_REWARD", 0x20: "BAD_INDEX",
                0x40: "SHIFT_REDO", 0x80: "BAD_GRAD", 0x100: "FILL_SHORT", 0x200: "SYNC_TIMEOUT"}

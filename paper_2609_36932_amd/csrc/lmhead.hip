@@ -126,8 +126,7 @@ constexpr int kGroupFwd = 32, kGroupDh = 4, kGroupDw = 4;
 // wavefront normally waits for a few hundred cycles at most)
 constexpr int kSyncSpins = 1 << 16;
 template <int MODE>
-__device__ __forceinline__ void tile_coords(int& mb, int& nb, int nmb, int nnb) {
-  const int b = blockIdx.x;
+__device__ __forceinline__ void tile_coords(int& mb, int& nb, int nmb, int nnb, int b) {
   constexpr int GROUP = MODE == MODE_FWD ? kGroupFwd : MODE == MODE_DH ? kGroupDh : kGroupDw;
   // the groups are vocab blocks in both dW forms: M blocks of MODE_DW, N blocks of MODE_DWT
   constexpr bool GN = MODE == MODE_DWT;
@@ -822,7 +821,7 @@ void lm_gemm_kernel(const GemmParams p) {
   __shared__ __attribute__((aligned(16))) char smem_raw[SmemBytes<T>::value];
   T* smem = reinterpret_cast<T*>(smem_raw);
   int mb, nb;
-  tile_coords<MODE>(mb, nb, p.nmb, p.nnb);
+  tile_coords<MODE>(mb, nb, p.nmb, p.nnb, blockIdx.x);
   if (MODE == MODE_FWD && p.store_e == 2 && p.redo_blk[nb] == 0) return;
   const int m0 = mb * kBM, n0 = nb * kBN;
   constexpr int NI = Geo<T, MODE>::NI, NT = Geo<T, MODE>::THREADS;
@@ -1014,6 +1013,34 @@ void lm_gemm_kernel(const GemmParams p) {
           }
         }
       }
+  }
+}
+
+// The two bf16 backward GEMMs of one slab in one launch: blocks [0, q.nmb q.nnb) are dhidden
+// tiles (K = padded vocabulary), the rest transposed-dW tiles (K = padded slab, about five times
+// shorter at the 7B shape).  Dispatched in block order, the dW tiles take the compute units that
+// the last partial wave of dhidden tiles leaves idle (a 27K-token slab has 5.8 waves of
+// dhidden tiles, a 19K-token slab at d = 1536 only 1.7).
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void lm_bwd_kernel(const GemmParams q, const GemmParams r) {
+  __shared__ __attribute__((aligned(16))) char smem_raw[SmemBytes<uint16_t>::value];
+  uint16_t* smem = reinterpret_cast<uint16_t*>(smem_raw);
+  const int nh = q.nmb * q.nnb;
+  const int b = blockIdx.x;
+  int mb, nb;
+  f32x4_t acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  if (b < nh) {
+    tile_coords<MODE_DH>(mb, nb, q.nmb, q.nnb, b);
+    mainloop_bf16_dma<MODE_DH>(q, mb * kBM, nb * kBN, acc, smem);
+    dh_epilogue_bf16(q, mb * kBM, nb * kBN, acc);
+  } else {
+    tile_coords<MODE_DWT>(mb, nb, r.nmb, r.nnb, b - nh);
+    mainloop_bf16_dma<MODE_DWT>(r, mb * kBM, nb * kBN, acc, smem);
+    dwt_epilogue_bf16(r, mb * kBM, nb * kBN, acc);
   }
 }
 
@@ -1587,6 +1614,24 @@ static int launch_gemm(GemmParams p, int kind, double flops, hipStream_t stream)
   return FASTRL_OK;
 }
 
+// dhidden (q, MODE_DH) and transposed dW (r, MODE_DWT) of one bf16 slab in one launch
+static int launch_bwd(GemmParams q, GemmParams r, double flops, hipStream_t stream) {
+  q.nmb = int((q.M + kBM - 1) / kBM);
+  q.nnb = int((q.N + kBN - 1) / kBN);
+  r.nmb = int((r.M + kBM - 1) / kBM);
+  r.nnb = int((r.N + kBN - 1) / kBN);
+  const int64_t nh = int64_t(q.nmb) * q.nnb, nw = int64_t(r.nmb) * r.nnb;
+  if (nh + nw == 0) return FASTRL_OK;
+  FR_CHECK_ARG(nh + nw < (int64_t(1) << 31), FASTRL_ERR_UNSUPPORTED, "backward GEMMs: grid too large");
+  FR_CHECK_ARG(r.K % 64 == 0 && r.ldb >= int64_t(r.nnb) * kBN && r.ldb % 8 == 0 && r.d % 4 == 0 &&
+                   r.M == r.d,
+               FASTRL_ERR_UNSUPPORTED, "transposed dW GEMM: unsupported shape");
+  ProfScope prof(FASTRL_K_BACKWARD, stream, flops);
+  hipLaunchKernelGGL(lm_bwd_kernel, dim3(unsigned(nh + nw)), dim3(512), 0, stream, q, r);
+  FR_LAUNCHED();
+  return FASTRL_OK;
+}
+
 #define FR_TRY(x)                 \
   do {                            \
     int rc_ = (x);                \
@@ -1937,8 +1982,8 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
                        a.beta, w.shift, w.gslab, w.cslab, w.seq_loss, w.seq_clip, a.status,
                        a.seq_index ? INT32_MAX : a.S);
     FR_LAUNCHED();
+    GemmParams q{};  // dhidden: C = E W^T (rows = tokens, cols = d, K = padded vocabulary)
     if (dh) {
-      GemmParams q{};
       q.A = w.E1; q.lda = Vpad; q.M = Tc;
       q.B = w.WT; q.ldb = Vpad; q.N = d;
       q.K = int32_t(Vpad);
@@ -1948,8 +1993,11 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
       q.dH_bf16 = a.dhidden_dtype == FASTRL_BF16;
       q.gslab = w.gslab; q.cslab = w.cslab; q.yslab = w.yslab; q.W = a.W; q.d = d;
       q.status = a.status;
-      FR_TRY((launch_gemm<T, MODE_DH>(q, FASTRL_K_DHIDDEN, 2.0 * double(Tc) * d * V, stream)));
     }
+    // bf16 with both gradients: the two GEMMs run as one launch (after dW's inputs are ready)
+    const bool fused = dh && dw && sizeof(T) == 2;
+    if (dh && !fused)
+      FR_TRY((launch_gemm<T, MODE_DH>(q, FASTRL_K_DHIDDEN, 2.0 * double(Tc) * d * V, stream)));
     if (dw) {
       dim3 g(nb1d(d, 64), unsigned(Tr / 64));
       hipLaunchKernelGGL((transpose_scale_kernel<T>), g, dim3(256), 0, stream,
@@ -1985,19 +2033,22 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
       hipLaunchKernelGGL(label_tok_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream,
                          w.lab_key, Tc, w.lab_tok);
       FR_LAUNCHED();
-      GemmParams q{};
-      q.K = int32_t(Tr);
-      q.dW = a.dW; q.dW_acc = (dw_written || a.dW_accumulate) ? 1 : 0;
-      q.d = d;
-      q.status = a.status;
+      GemmParams r{};
+      r.K = int32_t(Tr);
+      r.dW = a.dW; r.dW_acc = (dw_written || a.dW_accumulate) ? 1 : 0;
+      r.d = d;
+      r.status = a.status;
       if constexpr (sizeof(T) == 2) {  // dW^T = Bd E: A = Bd, B = E1 read K-major
-        q.A = w.Bd; q.lda = tcp; q.M = d;
-        q.B = w.E1; q.ldb = Vpad; q.N = V;
-        FR_TRY((launch_gemm<T, MODE_DWT>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
+        r.A = w.Bd; r.lda = tcp; r.M = d;
+        r.B = w.E1; r.ldb = Vpad; r.N = V;
+        if (fused)
+          FR_TRY(launch_bwd(q, r, 4.0 * double(V) * d * Tc, stream));
+        else
+          FR_TRY((launch_gemm<T, MODE_DWT>(r, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
       } else {  // dW = E^T Bd^T: A = E1 read K-major (A[v][t] = E1[t][v]), B = Bd
-        q.A = w.E1; q.lda = Vpad; q.M = V;
-        q.B = w.Bd; q.ldb = tcp; q.N = d;
-        FR_TRY((launch_gemm<T, MODE_DW>(q, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
+        r.A = w.E1; r.lda = Vpad; r.M = V;
+        r.B = w.Bd; r.ldb = tcp; r.N = d;
+        FR_TRY((launch_gemm<T, MODE_DW>(r, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
       }
       dw_written = true;
       const unsigned nch = unsigned((Tc + kOneHotChunk - 1) / kOneHotChunk);

@@ -211,10 +211,13 @@ def test_large_logits_take_the_shifted_path(fr):
                 dg=ref["dg"], lse=pb.lse_exact)
 
 
-def test_deterministic(fr):
+@pytest.mark.parametrize("slab", [0, 120])
+def test_deterministic(fr, slab):
+    """Two runs give the same bits: masks and offsets, the loss, dhidden and dW (with several
+    slabs, dW accumulated across them in the same order)."""
     pb = Problem(5, DEV, Q=4, len_range=(30, 80), V=800, d=64)
-    a = pb.run_gpu(fr)
-    b = pb.run_gpu(fr)
+    a = pb.run_gpu(fr, slab_tokens=slab)
+    b = pb.run_gpu(fr, slab_tokens=slab)
     torch.cuda.synchronize()
     nk, tk = a["n_kept"], a["t_kept"]
     assert (nk, tk) == (b["n_kept"], b["t_kept"])

@@ -2,7 +2,8 @@
 flags (no GPU needed).
 
 The K-major B fragments of the transposed dW GEMM are read with ds_read_b64_tr_b16 issued as
-inline assembly, which the compiler does not track: the kernel waits for those reads itself
+inline assembly (in the dW kernel and in the launch that runs dhidden and dW together), which
+the compiler does not track: the kernel waits for those reads itself
 (s_waitcnt lgkmcnt(0)).  On every control-flow path from such a read to the next full LDS
 wait, no instruction may read or write the read's destination registers (a copy or a use
 before the wait would see stale data).  Packed fp32 VALU instructions are kept out of every
@@ -18,6 +19,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_36932_amd", "csrc")
 DWT_KERNEL = "_ZN6fastrl14lm_gemm_kernelItLi3EEEvNS_10GemmParamsE"  # bf16, transposed dW
+BWD_KERNEL = "_ZN6fastrl13lm_bwd_kernelENS_10GemmParamsES0_"       # dhidden + transposed dW
+KERNELS_WITH_TR_READS = [DWT_KERNEL, BWD_KERNEL]
 REG = re.compile(r"\b([va])(\d+)\b|\b([va])\[(\d+):(\d+)\]")
 LABEL = re.compile(r"^(\.?[A-Za-z_][\w.$]*):")
 
@@ -126,8 +129,9 @@ def lmhead_asm(tmp_path_factory):
     return _compile(os.path.join(CSRC, "lmhead.hip"), tmp_path_factory.mktemp("asm"))
 
 
-def test_transposing_reads_are_waited_for_before_use(lmhead_asm):
-    lines = _body(lmhead_asm, DWT_KERNEL)
+@pytest.mark.parametrize("kernel", KERNELS_WITH_TR_READS)
+def test_transposing_reads_are_waited_for_before_use(lmhead_asm, kernel):
+    lines = _body(lmhead_asm, kernel)
     reads = [k for k, (kind, op, _) in enumerate(lines) if op == "ds_read_b64_tr_b16"]
     # two per B fragment, four fragments, three places (prologue, loop, last tile) at least
     assert len(reads) >= 24, len(reads)
@@ -138,10 +142,11 @@ def test_transposing_reads_are_waited_for_before_use(lmhead_asm):
         assert not bad, (lines[k], bad[:5])
 
 
-def test_transposing_read_pairs_fill_one_operand(lmhead_asm):
+@pytest.mark.parametrize("kernel", KERNELS_WITH_TR_READS)
+def test_transposing_read_pairs_fill_one_operand(lmhead_asm, kernel):
     """The two halves of a fragment land in adjacent registers, so the MFMA reads them in
     place (no copy that could run before the data arrives)."""
-    lines = _body(lmhead_asm, DWT_KERNEL)
+    lines = _body(lmhead_asm, kernel)
     dests = [sorted(_regs(args.split(",")[0])) for kind, op, args in lines
              if op == "ds_read_b64_tr_b16"]
     mfma_b = set()
