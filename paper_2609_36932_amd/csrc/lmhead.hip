@@ -708,29 +708,41 @@ __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, i
   }
   __syncthreads();
   if (!rel) {
+    // sums relative to the block's column max M: exp(z - M) = exp2(z log2e - M log2e), one FMA
+    // and one v_exp_f32 per logit; as in the stored-exp pass, full vocab blocks skip the row
+    // test and the z-weighted sum is only formed when the entropy is asked for
+    auto pass = [&](auto full_c, auto z_c) {
+      constexpr bool FULL = decltype(full_c)::value, WZ = decltype(z_c)::value;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int cl = wn * 64 + j * 16 + c;
-      const float M = fmaxf(xmax[cl], xmax[kBN + cl]);
-      float ssp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, zsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int j = 0; j < 4; ++j) {
+        const int cl = wn * 64 + j * 16 + c;
+        const float ml = fmaxf(xmax[cl], xmax[kBN + cl]) * 1.4426950408889634f;
+        float ssp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, zsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (rbase + 16 * i + q < Vr) {
-            const float ex = __expf(acc[i][j][q] - M);
+          for (int q = 0; q < 4; ++q) {
+            float ex = __builtin_amdgcn_exp2f(fmaf(acc[i][j][q], 1.4426950408889634f, -ml));
+            if (!FULL && rbase + 16 * i + q >= Vr) ex = 0.0f;
             ssp[i & 3] += ex;
-            zsp[i & 3] = fmaf(ex, acc[i][j][q], zsp[i & 3]);
+            if (WZ) zsp[i & 3] = fmaf(ex, acc[i][j][q], zsp[i & 3]);
           }
+        float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
+        ssum = group_sum4(ssum);
+        if (g == 0) xsum[wm * kBN + cl] = ssum;
+        if constexpr (WZ) {
+          float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
+          zsum = group_sum4(zsum);
+          if (g == 0) xsz[wm * kBN + cl] = zsum;
         }
-      float ssum = (ssp[0] + ssp[1]) + (ssp[2] + ssp[3]);
-      float zsum = (zsp[0] + zsp[1]) + (zsp[2] + zsp[3]);
-      ssum = group_sum4(ssum);
-      zsum = group_sum4(zsum);
-      if (g == 0) {
-        xsum[wm * kBN + cl] = ssum;
-        xsz[wm * kBN + cl] = zsum;
       }
+    };
+    if (rows_full) {
+      if (p.psz) pass(std::true_type{}, std::true_type{});
+      else pass(std::true_type{}, std::false_type{});
+    } else {
+      if (p.psz) pass(std::false_type{}, std::true_type{});
+      else pass(std::false_type{}, std::false_type{});
     }
     __syncthreads();
   }
