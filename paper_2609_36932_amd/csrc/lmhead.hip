@@ -16,13 +16,14 @@
 //        E1[t][v] = exp(z - s_t) (s_t = 0 unless exp(z) would leave float range).
 //   merge   partials -> lse, logp, row max; rows whose max is too far from s_t get
 //           s_t = max_t and their token block is evaluated again (rare), then merge again.
-//   loss    g_t and c_t = g_t exp(s_t - lse_t) per token (one block per sequence).
-//   DH   C = E1 . W^T  (rows = tokens, cols = d, K = vocab):
-//        dH[t] = g_t W[y_t] - c_t C[t].
+//   loss    g_t and c_t = g_t exp(s_t - lse_t) per token (one block per sequence).  With a
+//           backward it also folds the one-hot term into the exp-logits: since
+//           g_t = c_t exp(lse_t - s_t), E1[t][y_t] -= exp(lse_t - s_t) makes
+//           c_t E1[t][v] = g_t (P[t][v] - [v = y_t]) = -dZ[t][v] for every v.
+//   DH   C = E1 . W^T  (rows = tokens, cols = d, K = vocab):  dH[t] = -c_t C[t].
 //   DW   with Bd[n][t] = c_t H[t][n] (K = tokens; E1 is read K-major through transposing LDS
 //        reads): bf16 computes C' = Bd . E1 (rows = d, cols = vocab), f32 computes
-//        C = E1^T . Bd^T (rows = vocab, cols = d):
-//        dW[v] (+)= -C[v] + sum_{t in slab, y_t = v} g_t H[t].
+//        C = E1^T . Bd^T (rows = vocab, cols = d):  dW[v] (+)= -C[v].
 // Nothing of size [T, V] exists: the exp-logit buffer holds one slab, [slab, V], and the
 // default slab (32768 tokens) does not grow with T.
 #include <algorithm>
@@ -104,9 +105,7 @@ struct GemmParams {
   // ---- DH epilogue
   void* dH;                 // [.., d] at slab offset
   int32_t dH_bf16;
-  const float* gslab;       // [slab]
   const float* cslab;       // [slab]
-  const void* W;            // [V, d]   (labels' rows)
   int32_t d;
   // ---- DW epilogue
   float* dW;                // [V, d]
@@ -758,27 +757,25 @@ __device__ __forceinline__ void fwd_epilogue_bf16(const GemmParams& p, int m0, i
 
 
 // Epilogue of the bf16 dhidden GEMM on the 16 x 16 layout (acc[i][j]: token rows wm*128 + 16 i
-// + 4 (l / 16) + q, hidden columns wn*64 + 16 j + l % 16): dH[t] = g_t W[y_t] - c_t C[t].
+// + 4 (l / 16) + q, hidden columns wn*64 + 16 j + l % 16): dH[t] = -c_t C[t] (the one-hot term
+// is already in E1).
 __device__ __forceinline__ void dh_epilogue_bf16(const GemmParams& p, int m0, int n0,
                                                  f32x4_t (&acc)[8][4]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 2, wn = wave & 3;
   const int g = lane >> 4, c = lane & 15;
-  const uint16_t* Wg = static_cast<const uint16_t*>(p.W);
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int t = m0 + wm * 128 + 16 * i + 4 * g + q;
       if (t < p.M) {
-        const int y = p.yslab[t];
-        const float gt = p.gslab[t], ct = p.cslab[t];
+        const float ct = p.cslab[t];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int n = n0 + wn * 64 + 16 * j + c;
           if (n < p.N) {
-            const float wy = y >= 0 ? bf16_to_f32(Wg[int64_t(y) * p.d + n]) : 0.0f;
-            const float val = gt * wy - ct * acc[i][j][q];
+            const float val = -ct * acc[i][j][q];
             const int64_t o = int64_t(t) * p.d + n;
             if (p.dH_bf16) static_cast<uint16_t*>(p.dH)[o] = f32_to_bf16(val);
             else static_cast<float*>(p.dH)[o] = val;
@@ -791,8 +788,8 @@ __device__ __forceinline__ void dh_epilogue_bf16(const GemmParams& p, int m0, in
 // Epilogue of the bf16 dW GEMM computed transposed (C' = Bd E on the 16 x 16 layout: acc[i][j]
 // holds hidden columns n = wm*128 + 16 i + 4 (l / 16) + q of vocab row v = wn*64 + 16 j + l % 16):
 // each lane owns 4 consecutive n of one dW row and moves them as one 16-byte access.
-// dW[v][n] (+)= -C'[n][v]; the one-hot part is added by dw_onehot_kernel.  Needs d % 4 == 0 and
-// a 16-byte aligned dW (checked on the host).
+// dW[v][n] (+)= -C'[n][v] (the one-hot term is already in E1).  Needs d % 4 == 0 and a 16-byte
+// aligned dW (checked on the host).
 __device__ __forceinline__ void dwt_epilogue_bf16(const GemmParams& p, int m0, int n0,
                                                   f32x4_t (&acc)[8][4]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -974,22 +971,19 @@ void lm_gemm_kernel(const GemmParams p) {
         if (p.psz) p.psz[int64_t(mb) * p.ldp + t] = xsz[cl] + xsz[kBN + cl];
       }
     }
-  } else if constexpr (MODE == MODE_DH && !Geo<T, MODE>::W8) {
-    const T* Wg = static_cast<const T*>(p.W);
+  } else if constexpr (MODE == MODE_DH && !Geo<T, MODE>::W8) {  // dH[t] = -c_t C[t]
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int t = m0 + acc_row(wm, mi, r, lane);
         if (t < p.M) {
-          const int y = p.yslab[t];
-          const float g = p.gslab[t], c = p.cslab[t];
+          const float c = p.cslab[t];
 #pragma unroll
           for (int ni = 0; ni < NI; ++ni) {
             const int n = n0 + acc_col<T, MODE>(wn, ni, lane);
             if (n < p.N) {
-              const float wy = y >= 0 ? to_f32<T>(Wg[int64_t(y) * p.d + n]) : 0.0f;
-              const float val = g * wy - c * acc[mi][ni][r];
+              const float val = -c * acc[mi][ni][r];
               const int64_t o = int64_t(t) * p.d + n;
               if (p.dH_bf16) static_cast<uint16_t*>(p.dH)[o] = f32_to_bf16(val);
               else static_cast<float*>(p.dH)[o] = val;
@@ -997,7 +991,7 @@ void lm_gemm_kernel(const GemmParams p) {
           }
         }
       }
-  } else {  // MODE_DW: dW[v] (+)= -C[v]; the one-hot part is added by dw_onehot_kernel
+  } else {  // MODE_DW: dW[v] (+)= -C[v] (the one-hot term is already in E1)
     // RB rows at a time
     constexpr int RB = 4;
 #pragma unroll
@@ -1183,7 +1177,8 @@ __device__ __forceinline__ double block_sum_d(double v, double* red) {
   return s;
 }
 
-// one block per sequence of the slab: g_t, c_t and the sequence's loss term
+// one block per sequence of the slab: g_t, c_t, the sequence's loss term and, with a backward,
+// the one-hot term of each token folded into its exp-logit row
 __global__ __launch_bounds__(256) void loss_kernel(
     const float* __restrict__ logp, const float* __restrict__ lse,
     const float* __restrict__ old_logp, const float* __restrict__ ref_logp,
@@ -1191,8 +1186,9 @@ __global__ __launch_bounds__(256) void loss_kernel(
     const float* __restrict__ adv, const int32_t* __restrict__ seq_index, int32_t S,
     int64_t T, int32_t seq_begin, int64_t row_base, int32_t algo, int32_t norm,
     float eps_low, float eps_high, float beta, const float* __restrict__ shift,
-    float* __restrict__ gslab, float* __restrict__ cslab, double* __restrict__ seq_loss,
-    int32_t* __restrict__ seq_clip, int32_t* __restrict__ status, int32_t nadv) {
+    float* __restrict__ cslab, double* __restrict__ seq_loss,
+    int32_t* __restrict__ seq_clip, int32_t* __restrict__ status, int32_t nadv,
+    void* __restrict__ E1, int64_t ldE1, int32_t e_bf16, const int32_t* __restrict__ yslab) {
   __shared__ double red[4];
   __shared__ double redc[4];
   const int i = seq_begin + blockIdx.x;
@@ -1248,9 +1244,22 @@ __global__ __launch_bounds__(256) void loss_kernel(
       g += double(beta) * w * (1.0 - e);
     }
     const int64_t tl = t - row_base;
-    gslab[tl] = float(g);
     const float s_t = shift ? shift[tl] : 0.0f;
     cslab[tl] = float(g * exp(double(s_t) - double(lse[t])));
+    // one-hot term of dZ folded into the exp-logits for the backward GEMMs: with
+    // g_t = c_t exp(lse_t - s_t), c_t (E1[t][y_t] - exp(lse_t - s_t)) = c_t E1[t][y_t] - g_t
+    const int y = E1 ? yslab[tl] : -1;
+    if (y >= 0) {
+      const double corr = exp(double(lse[t]) - double(s_t));
+      const int64_t o = tl * ldE1 + y;
+      if (e_bf16) {
+        uint16_t* e = static_cast<uint16_t*>(E1) + o;
+        *e = f32_to_bf16(float(double(bf16_to_f32(*e)) - corr));
+      } else {
+        float* e = static_cast<float*>(E1) + o;
+        *e = float(double(*e) - corr);
+      }
+    }
   }
   kpart = block_sum_d(kpart, red);
   const double clips = block_sum_d(algo == FASTRL_GSPO ? 0.0 : double(clip), redc);
@@ -1347,258 +1356,6 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
   for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * blockDim.x)
     p[i] = v;
-}
-
-__global__ void label_hist_kernel(const int32_t* __restrict__ yslab, int32_t Tc,
-                                  int32_t* __restrict__ cnt) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < Tc && yslab[t] >= 0) atomicAdd(&cnt[yslab[t]], 1);
-}
-
-// exclusive scan of cnt[0..n) into off[0..n]: one block, 8 consecutive counts per thread, so
-// a pass covers 8192 counts (19 passes at a 152K vocabulary)
-__global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ cnt, int32_t n,
-                                                    int32_t* __restrict__ off) {
-  constexpr int E = 8;
-  __shared__ int32_t ws[16];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  int32_t base = 0;
-  for (int c = 0; c < n; c += 1024 * E) {
-    const int i0 = c + tid * E;
-    int x[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) x[e] = i0 + e < n ? cnt[i0 + e] : 0;
-    int tsum = 0;
-#pragma unroll
-    for (int e = 0; e < E; ++e) tsum += x[e];
-    int v = tsum;  // inclusive scan of the thread sums over the wavefront
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int t = __shfl_up(v, o, 64);
-      if (lane >= o) v += t;
-    }
-    if (lane == 63) ws[wv] = v;
-    __syncthreads();
-    int pre = 0, tot = 0;
-    for (int w = 0; w < 16; ++w) {
-      if (w < wv) pre += ws[w];
-      tot += ws[w];
-    }
-    int run = base + pre + v - tsum;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      if (i0 + e < n) off[i0 + e] = run;
-      run += x[e];
-    }
-    base += tot;
-    __syncthreads();
-  }
-  if (tid == 0) off[n] = base;
-}
-
-// ---- label CSR: the slab's labelled tokens ordered by (label, token) ----------------------
-// Keys (label << 32 | token) are sorted with a bitonic network, so the order inside a label
-// is the token order whatever the label distribution (one token id can fill a large part of
-// a slab of real text).  n is a power of two >= kSortTile; unlabelled tokens and the padding
-// carry the largest key and sort to the end.
-constexpr int kSortTile = 2048;  // keys per block in the LDS stages (1024 threads, 16 KB)
-
-__global__ void label_key_kernel(const int32_t* __restrict__ yslab, int32_t Tc, int64_t n,
-                                 uint64_t* __restrict__ key) {
-  const int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
-  if (i >= n) return;
-  const int y = i < Tc ? yslab[i] : -1;
-  key[i] = y >= 0 ? (uint64_t(uint32_t(y)) << 32) | uint64_t(i) : ~uint64_t(0);
-}
-
-// compare-exchange of positions i and i + j inside one LDS tile; the direction of the
-// sequence being built is ascending where bit k of the global position is clear
-__device__ __forceinline__ void bitonic_cx(uint64_t* s, int64_t base, int i, int j, int64_t k) {
-  const uint64_t a = s[i], b = s[i + j];
-  const bool asc = ((base + i) & k) == 0;
-  if (asc ? a > b : a < b) {
-    s[i] = b;
-    s[i + j] = a;
-  }
-}
-
-// k_merge == 0: sort every tile (stages k = 2 .. kSortTile); otherwise the steps j < kSortTile
-// of stage k_merge
-__global__ __launch_bounds__(1024) void bitonic_tile_kernel(uint64_t* __restrict__ key,
-                                                            int64_t k_merge) {
-  __shared__ uint64_t s[kSortTile];
-  const int tid = threadIdx.x;
-  const int64_t base = int64_t(blockIdx.x) * kSortTile;
-  s[tid] = key[base + tid];
-  s[tid + kSortTile / 2] = key[base + tid + kSortTile / 2];
-  __syncthreads();
-  auto steps = [&](int64_t k, int j0) {
-    for (int j = j0; j > 0; j >>= 1) {
-      bitonic_cx(s, base, (tid / j) * 2 * j + tid % j, j, k);
-      __syncthreads();
-    }
-  };
-  if (k_merge == 0) {
-    for (int k = 2; k <= kSortTile; k <<= 1) steps(k, k >> 1);
-  } else {
-    steps(k_merge, kSortTile / 2);
-  }
-  key[base + tid] = s[tid];
-  key[base + tid + kSortTile / 2] = s[tid + kSortTile / 2];
-}
-
-// one step j >= kSortTile of stage k, over all n / 2 pairs
-__global__ void bitonic_step_kernel(uint64_t* __restrict__ key, int64_t n, int64_t k, int64_t j) {
-  const int64_t p = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
-  if (p >= n / 2) return;
-  const int64_t i = (p / j) * 2 * j + p % j;
-  const uint64_t a = key[i], b = key[i + j];
-  const bool asc = (i & k) == 0;
-  if (asc ? a > b : a < b) {
-    key[i] = b;
-    key[i + j] = a;
-  }
-}
-
-__global__ void label_tok_kernel(const uint64_t* __restrict__ key, int32_t Tc,
-                                 int32_t* __restrict__ lab_tok) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < Tc && key[i] != ~uint64_t(0)) lab_tok[i] = int32_t(uint32_t(key[i]));
-}
-
-// One-hot part of dW for one slab: dW[v] += sum over the slab tokens t labelled v of g_t H[t],
-// as a segmented sum over the label CSR in fixed chunks of kOneHotChunk positions (one block
-// per chunk, four consecutive columns per thread).  A label whose tokens all lie in the chunk
-// is added to dW by the chunk; a label cut by a chunk edge leaves its chunk partials (the part
-// after the edge in `head`, the part before it in `tail`) for dw_onehot_carry_kernel, which
-// adds them in chunk order.  Every sum has a fixed order, so dW is deterministic, and the work
-// per block is bounded however the labels are distributed.
-constexpr int kOneHotChunk = 128;
-
-template <typename T>
-__device__ __forceinline__ void load4(const T* p, float (&v)[4]);
-template <>
-__device__ __forceinline__ void load4<uint16_t>(const uint16_t* p, float (&v)[4]) {
-  const uint2 u = *reinterpret_cast<const uint2*>(p);
-  v[0] = __uint_as_float(u.x << 16);
-  v[1] = __uint_as_float(u.x & 0xffff0000u);
-  v[2] = __uint_as_float(u.y << 16);
-  v[3] = __uint_as_float(u.y & 0xffff0000u);
-}
-template <>
-__device__ __forceinline__ void load4<float>(const float* p, float (&v)[4]) {
-  const float4 u = *reinterpret_cast<const float4*>(p);
-  v[0] = u.x;
-  v[1] = u.y;
-  v[2] = u.z;
-  v[3] = u.w;
-}
-
-__device__ __forceinline__ void add4(float* __restrict__ p, const float (&s)[4]) {
-  float4 w = *reinterpret_cast<float4*>(p);
-  w.x += s[0];
-  w.y += s[1];
-  w.z += s[2];
-  w.w += s[3];
-  *reinterpret_cast<float4*>(p) = w;
-}
-
-template <typename T>
-__global__ __launch_bounds__(256) void dw_onehot_kernel(
-    const int32_t* __restrict__ lab_off, const int32_t* __restrict__ lab_tok,
-    const int32_t* __restrict__ yslab, const float* __restrict__ gslab, const T* __restrict__ H,
-    const int32_t* __restrict__ row_index, int64_t row_base, int32_t d, int32_t V,
-    float* __restrict__ dW, float* __restrict__ head, float* __restrict__ tail) {
-  __shared__ int64_t srow[kOneHotChunk];
-  __shared__ float sg[kOneHotChunk];
-  __shared__ int32_t sy[kOneHotChunk], sflag[kOneHotChunk];
-  const int nvalid = lab_off[V];
-  const int lo = blockIdx.x * kOneHotChunk;
-  if (lo >= nvalid) return;
-  const int cnt = min(kOneHotChunk, nvalid - lo), hi = lo + cnt;
-  for (int i = threadIdx.x; i < cnt; i += blockDim.x) {
-    const int t = lab_tok[lo + i];
-    const int y = yslab[t];
-    int64_t row = row_base + t;
-    if (row_index) row = row_index[row];
-    srow[i] = row;
-    sg[i] = gslab[t];
-    sy[i] = y;
-    // bit 0: last position of its label in the chunk; bit 1: the label starts in the chunk;
-    // bit 2: it ends in the chunk
-    const bool last = i + 1 == cnt || yslab[lab_tok[lo + i + 1]] != y;
-    sflag[i] = (last ? 1 : 0) | (lab_off[y] >= lo ? 2 : 0) | (lab_off[y + 1] <= hi ? 4 : 0);
-  }
-  __syncthreads();
-  // U positions per batch: their H rows, and the dW rows of the labels that end inside the
-  // chunk at them, are loaded before any of them is used (with one label per position, as
-  // in a near-uniform distribution, every position ends a label)
-  constexpr int U = 8;
-  for (int n0 = threadIdx.x * 4; n0 < d; n0 += blockDim.x * 4) {
-    float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int i0 = 0; i0 < cnt; i0 += U) {
-      float h[U][4], w[U][4];
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (i0 + u < cnt) {
-          load4<T>(H + srow[i0 + u] * d + n0, h[u]);
-          if (sflag[i0 + u] == 7) load4<float>(dW + int64_t(sy[i0 + u]) * d + n0, w[u]);
-        }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int i = i0 + u;
-        if (i >= cnt) break;
-        const float g = sg[i];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) s[q] += g * h[u][q];
-        const int f = sflag[i];
-        if (f & 1) {
-          if (f == 7) {
-            *reinterpret_cast<float4*>(dW + int64_t(sy[i]) * d + n0) =
-                make_float4(w[u][0] + s[0], w[u][1] + s[1], w[u][2] + s[2], w[u][3] + s[3]);
-          } else {
-            float* c = ((f & 2) ? tail : head) + int64_t(blockIdx.x) * d + n0;
-            *reinterpret_cast<float4*>(c) = make_float4(s[0], s[1], s[2], s[3]);
-          }
-#pragma unroll
-          for (int q = 0; q < 4; ++q) s[q] = 0.0f;
-        }
-      }
-    }
-  }
-}
-
-// labels cut by chunk edges: the chunk where such a label starts adds its own tail partial and
-// the head partials of the following chunks up to the one where the label ends
-__global__ __launch_bounds__(256) void dw_onehot_carry_kernel(
-    const int32_t* __restrict__ lab_off, const int32_t* __restrict__ lab_tok,
-    const int32_t* __restrict__ yslab, int32_t d, int32_t V, float* __restrict__ dW,
-    const float* __restrict__ head, const float* __restrict__ tail) {
-  const int nvalid = lab_off[V];
-  const int lo = blockIdx.x * kOneHotChunk;
-  if (lo >= nvalid) return;
-  const int hi = min(lo + kOneHotChunk, nvalid);
-  const int y = yslab[lab_tok[hi - 1]];
-  const int a = lab_off[y], b = lab_off[y + 1];
-  if (a < lo || b <= hi) return;  // the chunk's last label starts before it or ends in it
-  const int c1 = (b - 1) / kOneHotChunk;
-  for (int n0 = threadIdx.x * 4; n0 < d; n0 += blockDim.x * 4) {
-    float s[4];
-    load4<float>(tail + int64_t(blockIdx.x) * d + n0, s);
-    for (int c0 = blockIdx.x + 1; c0 <= c1; c0 += 8) {  // 8 loads in flight, added in order
-      float h[8][4];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (c0 + u <= c1) load4<float>(head + int64_t(c0 + u) * d + n0, h[u]);
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (c0 + u <= c1) {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) s[q] += h[u][q];
-        }
-    }
-    add4(dW + int64_t(y) * d + n0, s);
-  }
 }
 
 // ------------------------------------------------------------------ host side
@@ -1841,19 +1598,10 @@ static SlabPlan plan_slabs(const int64_t* off, int32_t S, int64_t cap) {
 
 struct LossWs {
   void *WT, *E1, *Bd;
-  float *pmax, *psum, *psz, *ent, *zlab, *shift, *gslab, *cslab, *lse, *logp;
-  int32_t *yslab, *redo_blk, *redo_count, *seq_clip, *lab_cnt, *lab_off, *lab_tok;
-  uint64_t* lab_key;
-  float *oh_head, *oh_tail;
+  float *pmax, *psum, *psz, *ent, *zlab, *shift, *cslab, *lse, *logp;
+  int32_t *yslab, *redo_blk, *redo_count, *seq_clip;
   double* seq_loss;
 };
-
-// length of the label sort: a power of two >= max(n, kSortTile)
-static int64_t sort_len(int64_t n) {
-  int64_t m = kSortTile;
-  while (m < n) m <<= 1;
-  return m;
-}
 
 static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_t tc_max) {
   const int esz = a.dtype == FASTRL_BF16 ? 2 : 4;
@@ -1872,7 +1620,6 @@ static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_
                     : (a.entropy_sum ? c.take<float>(size_t(std::max<int64_t>(a.T, 1))) : nullptr);
   w.zlab = c.take<float>(size_t(tcp));
   w.shift = c.take<float>(size_t(tcp));
-  w.gslab = c.take<float>(size_t(tcp));
   w.cslab = c.take<float>(size_t(tcp));
   w.yslab = c.take<int32_t>(size_t(tcp));
   w.redo_blk = c.take<int32_t>(size_t(tcp / kBN));
@@ -1881,13 +1628,6 @@ static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_
   w.logp = a.logp ? a.logp : c.take<float>(size_t(std::max<int64_t>(a.T, 1)));
   w.seq_loss = c.take<double>(size_t(std::max(a.S, 1)));
   w.seq_clip = c.take<int32_t>(size_t(std::max(a.S, 1)));
-  w.lab_cnt = c.take<int32_t>(size_t(a.V + 1));
-  w.lab_off = c.take<int32_t>(size_t(a.V + 1));
-  w.lab_tok = c.take<int32_t>(size_t(tcp));
-  w.lab_key = dw ? c.take<uint64_t>(size_t(sort_len(tcp))) : nullptr;
-  const int64_t nch = (tcp + kOneHotChunk - 1) / kOneHotChunk;
-  w.oh_head = dw ? c.take<float>(size_t(nch * a.d)) : nullptr;
-  w.oh_tail = dw ? c.take<float>(size_t(nch * a.d)) : nullptr;
   return c.size();
 }
 
@@ -1949,8 +1689,9 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
       hipLaunchKernelGGL(loss_kernel, dim3(unsigned(s1 - s0)), dim3(256), 0, stream, w.logp,
                          w.lse, a.old_logp, a.ref_logp, a.row_index, a.seq_off, a.adv,
                          a.seq_index, a.S, a.T, s0, t0, a.algo, a.norm, a.eps_low, a.eps_high,
-                         a.beta, w.shift, w.gslab, w.cslab, w.seq_loss, w.seq_clip, a.status,
-                         a.seq_index ? INT32_MAX : a.S);
+                         a.beta, w.shift, w.cslab, w.seq_loss, w.seq_clip, a.status,
+                         a.seq_index ? INT32_MAX : a.S, (void*)nullptr, int64_t(0), 0,
+                         (const int32_t*)nullptr);
       FR_LAUNCHED();
       continue;
     }
@@ -1991,8 +1732,9 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
     hipLaunchKernelGGL(loss_kernel, dim3(unsigned(s1 - s0)), dim3(256), 0, stream, w.logp,
                        w.lse, a.old_logp, a.ref_logp, a.row_index, a.seq_off, a.adv,
                        a.seq_index, a.S, a.T, s0, t0, a.algo, a.norm, a.eps_low, a.eps_high,
-                       a.beta, w.shift, w.gslab, w.cslab, w.seq_loss, w.seq_clip, a.status,
-                       a.seq_index ? INT32_MAX : a.S);
+                       a.beta, w.shift, w.cslab, w.seq_loss, w.seq_clip, a.status,
+                       a.seq_index ? INT32_MAX : a.S, store ? w.E1 : nullptr, Vpad,
+                       sizeof(T) == 2 ? 1 : 0, w.yslab);
     FR_LAUNCHED();
     GemmParams q{};  // dhidden: C = E W^T (rows = tokens, cols = d, K = padded vocabulary)
     if (dh) {
@@ -2003,7 +1745,7 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
                  ? (void*)(static_cast<uint16_t*>(a.dhidden) + t0 * d)
                  : (void*)(static_cast<float*>(a.dhidden) + t0 * d);
       q.dH_bf16 = a.dhidden_dtype == FASTRL_BF16;
-      q.gslab = w.gslab; q.cslab = w.cslab; q.yslab = w.yslab; q.W = a.W; q.d = d;
+      q.cslab = w.cslab; q.d = d;
       q.status = a.status;
     }
     // bf16 with both gradients: the two GEMMs run as one launch (after dW's inputs are ready)
@@ -2015,35 +1757,6 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
       hipLaunchKernelGGL((transpose_scale_kernel<T>), g, dim3(256), 0, stream,
                          static_cast<const T*>(a.hidden), a.row_index, t0, Tc, int32_t(Tr), d,
                          w.cslab, static_cast<T*>(w.Bd), tcp);
-      FR_LAUNCHED();
-      hipLaunchKernelGGL(fill_i32_kernel, dim3(256), dim3(256), 0, stream, w.lab_cnt,
-                         int64_t(V), 0);
-      FR_LAUNCHED();
-      hipLaunchKernelGGL(label_hist_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0,
-                         stream, w.yslab, Tc, w.lab_cnt);
-      FR_LAUNCHED();
-      hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, stream, w.lab_cnt, V, w.lab_off);
-      FR_LAUNCHED();
-      // label CSR in (label, token) order: bitonic sort of the slab's keys
-      const int64_t n = sort_len(Tc);
-      hipLaunchKernelGGL(label_key_kernel, dim3(unsigned(n / 256)), dim3(256), 0, stream,
-                         w.yslab, Tc, n, w.lab_key);
-      FR_LAUNCHED();
-      hipLaunchKernelGGL(bitonic_tile_kernel, dim3(unsigned(n / kSortTile)), dim3(1024), 0,
-                         stream, w.lab_key, int64_t(0));
-      FR_LAUNCHED();
-      for (int64_t k = 2 * kSortTile; k <= n; k <<= 1) {
-        for (int64_t j = k / 2; j >= kSortTile; j >>= 1) {
-          hipLaunchKernelGGL(bitonic_step_kernel, dim3(unsigned(n / 2 / 256)), dim3(256), 0,
-                             stream, w.lab_key, n, k, j);
-          FR_LAUNCHED();
-        }
-        hipLaunchKernelGGL(bitonic_tile_kernel, dim3(unsigned(n / kSortTile)), dim3(1024), 0,
-                           stream, w.lab_key, k);
-        FR_LAUNCHED();
-      }
-      hipLaunchKernelGGL(label_tok_kernel, dim3(nb1d(Tc, 256)), dim3(256), 0, stream,
-                         w.lab_key, Tc, w.lab_tok);
       FR_LAUNCHED();
       GemmParams r{};
       r.K = int32_t(Tr);
@@ -2063,14 +1776,6 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
         FR_TRY((launch_gemm<T, MODE_DW>(r, FASTRL_K_DW, 2.0 * double(V) * d * Tc, stream)));
       }
       dw_written = true;
-      const unsigned nch = unsigned((Tc + kOneHotChunk - 1) / kOneHotChunk);
-      hipLaunchKernelGGL((dw_onehot_kernel<T>), dim3(nch), dim3(256), 0, stream, w.lab_off,
-                         w.lab_tok, w.yslab, w.gslab, static_cast<const T*>(a.hidden),
-                         a.row_index, t0, d, V, a.dW, w.oh_head, w.oh_tail);
-      FR_LAUNCHED();
-      hipLaunchKernelGGL(dw_onehot_carry_kernel, dim3(nch), dim3(256), 0, stream, w.lab_off,
-                         w.lab_tok, w.yslab, d, V, a.dW, w.oh_head, w.oh_tail);
-      FR_LAUNCHED();
     }
   }
   hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, stream, w.seq_loss, w.seq_clip,

@@ -17,6 +17,10 @@ REL = 1e-2
 # every token (and GSPO sequence) ratio at least this far from a clip edge in log space, so
 # no clip decision flips within it (measured GPU log-prob errors are ~1e-5)
 G_LOGP_EPS = 1e-4
+# unit roundoff of the exp-logit operand of the backward GEMMs: bfloat16 (8 significant bits)
+# and float32
+BF16_U = 2.0 ** -8
+FP32_U = 2.0 ** -24
 
 
 def rel_fro(a, b):
@@ -43,6 +47,7 @@ class Problem:
         self.V = V or base.V
         self.d = d or base.d
         self.dtype = dtype or base.dtype
+        self.fold_u = FP32_U if self.dtype == "f32" else BF16_U
         self.keep_ratio = base.keep_ratio if keep_ratio is None else keep_ratio
         self.tau = (base.tau_num, base.tau_den) if tau is None else tau
         self.ngram_n = base.ngram_n if ngram_n is None else ngram_n
@@ -123,6 +128,30 @@ class Problem:
             slab_tokens=slab_tokens, status=status, dhidden_dtype=dhidden_dtype)
 
 
+def fold_bounds(H, W, y, g, u=BF16_U):
+    """Frobenius bounds of what the one-hot fold adds to the error of dhidden and of dW.  The
+    backward GEMMs take the one-hot term of dZ from the exp-logit operand: its label entry
+    E[t][y_t] - exp(lse_t - s_t) is rounded once to the operand's precision (unit roundoff u,
+    as in a dlogits operand of that type), and with E[t][y_t]'s own rounding the entry times
+    c_t moves by at most u |g_t| (|p_ty - 1| + p_ty = 1): u |g_t| ||W_{y_t}|| in dhidden row t,
+    sum_{t: y_t = v} u |g_t| ||H_t|| in dW row v."""
+    H = np.asarray(H, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    a = u * np.abs(np.asarray(g, dtype=np.float64))
+    bH = a * np.linalg.norm(W[y], axis=1)
+    bW = np.zeros(W.shape[0])
+    np.add.at(bW, y, a * np.linalg.norm(H, axis=1))
+    return float(np.sqrt((bH ** 2).sum())), float(np.sqrt((bW ** 2).sum()))
+
+
+def soft_excess(gpu, ref, part, bound, rel=REL):
+    """The softmax part alone (the reference minus its one-hot part): ||gpu - ref|| against
+    rel ||ref - part|| + bound (fold_bounds), as a ratio scaled by rel (<= rel passes)."""
+    num = np.linalg.norm(np.asarray(gpu, dtype=np.float64) - ref)
+    den = rel * np.linalg.norm(ref - part) + bound
+    return rel * (num / den if den > 0 else (0.0 if num == 0 else np.inf))
+
+
 def onehot_parts(H, W, y, g):
     """The sparse parts of the LM-head gradient: g_t W[y_t] (dH) and the scatter of
     g_t H_t onto row y_t (dW)."""
@@ -171,9 +200,11 @@ def row_tol_excess(gpu, ref, extra, rel):
     return float(r.max()) if len(r) else 0.0
 
 
-def check_grads(H, W, y, g_ref, dH_gpu, dW_gpu, dH_ref, dW_ref, rel=REL, dg=None, lse=None):
-    """Whole-gradient relative Frobenius error, the same for the softmax part alone (the
-    dense GEMM part; the one-hot part dominates the norm), and per row (every token's dhidden
+def check_grads(H, W, y, g_ref, dH_gpu, dW_gpu, dH_ref, dW_ref, rel=REL, dg=None, lse=None,
+                u=BF16_U):
+    """Whole-gradient relative Frobenius error; the softmax part alone (the one-hot part
+    dominates the norm) within rel of its norm plus the bound of the one-hot term's rounding
+    in the exp-logit operand (fold_bounds, unit roundoff u); and per row (every token's dhidden
     row, every vocabulary row of dW): ||gpu_r - ref_r|| <= rel ||ref_r|| + e_r, where e_r is
     what a per-token deviation dg of g (g_deviation: the oracle's g under a log-prob error of
     G_LOGP_EPS) moves that row by: dg_t ||W_{y_t} - sum_v p_tv W_v|| for dhidden row t and
@@ -191,15 +222,15 @@ def check_grads(H, W, y, g_ref, dH_gpu, dW_gpu, dH_ref, dW_ref, rel=REL, dg=None
         A[np.arange(T), y] += 1.0
         eH = np.asarray(dg) * np.linalg.norm(A @ W, axis=1)
         eW = np.abs(A).T @ (np.asarray(dg) * np.linalg.norm(H, axis=1))
+    bH, bW = fold_bounds(H, W, y, g_ref, u)
+    dH1, dW1 = onehot_parts(H, W, y, g_ref)
     if dH_gpu is not None:
         out["dH"] = rel_fro(dH_gpu, dH_ref)
-        dH1, _ = onehot_parts(H, W, y, g_ref)
-        out["dH_soft"] = rel_fro(dH_gpu - dH1, dH_ref - dH1)
+        out["dH_soft"] = soft_excess(dH_gpu, dH_ref, dH1, bH, rel)
         out["dH_row"] = row_tol_excess(dH_gpu, dH_ref, eH, rel) * rel
     if dW_gpu is not None:
         out["dW"] = rel_fro(dW_gpu, dW_ref)
-        _, dW1 = onehot_parts(H, W, y, g_ref)
-        out["dW_soft"] = rel_fro(dW_gpu - dW1, dW_ref - dW1)
+        out["dW_soft"] = soft_excess(dW_gpu, dW_ref, dW1, bW, rel)
         out["dW_row"] = row_tol_excess(dW_gpu, dW_ref, eW, rel) * rel
     for k, v in out.items():
         assert v <= rel, (k, v, out)

@@ -28,7 +28,7 @@ import torch
 
 import oracle
 from synth import CONFIGS, make_rollouts, make_dense
-from tests._parity import rel_fro, row_rel, onehot_parts, LOGP_ATOL, REL
+from tests._parity import rel_fro, row_rel, onehot_parts, fold_bounds, soft_excess, LOGP_ATOL, REL
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -139,7 +139,7 @@ def test_full_config(fr, c):
     dH_gpu = call.dhidden[torch.from_numpy(sample).long().to(DEV)].double().cpu().numpy()
     e1 = rel_fro(dH_gpu, dH_s)
     dH1, _ = onehot_parts(Hs, W64, y_all[sample], g_s)
-    e2 = rel_fro(dH_gpu - dH1, dH_s - dH1)
+    e2 = soft_excess(dH_gpu, dH_s, dH1, fold_bounds(Hs, W64, y_all[sample], g_s)[0])
     e3 = row_rel(dH_gpu, dH_s)
     assert np.abs(g_s).max() > 0 and e1 < REL and e2 < REL and e3 < REL, (e1, e2, e3)
     # the forward-only entry point (the old / ref passes) on the same kept tokens, full size
@@ -212,8 +212,9 @@ def test_full_config(fr, c):
     dHg = call2.dhidden[:T2].double().cpu().numpy()
     dWg = call2.dW.double().cpu().numpy()
     dH1, dW1 = onehot_parts(Hs2, W64, y_all[:T2], g2)
+    bH, bW = fold_bounds(Hs2, W64, y_all[:T2], g2)
     errs = dict(dH=rel_fro(dHg, dH2), dW=rel_fro(dWg, dW2),
-                dH_soft=rel_fro(dHg - dH1, dH2 - dH1), dW_soft=rel_fro(dWg - dW1, dW2 - dW1),
+                dH_soft=soft_excess(dHg, dH2, dH1, bH), dW_soft=soft_excess(dWg, dW2, dW1, bW),
                 dH_row=row_rel(dHg, dH2), dW_row=row_rel(dWg, dW2))
     print(f"[fullsize] cfg {c} slab of {S2} sequences / {T2} tokens: {errs}", flush=True)
     for k, v in errs.items():

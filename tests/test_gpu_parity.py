@@ -170,7 +170,7 @@ def test_hot_path_small(fr, case, slab):
     Hk = pb.H64[pb.src]
     errs = check_grads(Hk, pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
                        call.dW.double().cpu().numpy(), ref["dH"], ref["dW"],
-                dg=ref["dg"], lse=pb.lse_exact)
+                       dg=ref["dg"], lse=pb.lse_exact, u=pb.fold_u)
     print(case, slab, errs)
 
 
@@ -188,7 +188,7 @@ def test_cfg1_full(fr):
     assert abs(call.loss.item() - ref["loss"]) <= 1e-4 * abs(ref["loss"])
     check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
                 call.dW.double().cpu().numpy(), ref["dH"], ref["dW"], rel=1e-4, dg=pb.g_dev(1e-6),
-                lse=pb.lse_exact)
+                lse=pb.lse_exact, u=pb.fold_u)
 
 
 def test_large_logits_take_the_shifted_path(fr):
@@ -232,9 +232,9 @@ def test_deterministic(fr, slab):
 @pytest.mark.parametrize("skew", [0.7, 1.0])
 @pytest.mark.parametrize("slab", [0, 1000])
 def test_head_heavy_labels(fr, skew, slab):
-    """A token distribution where one id fills most positions (1.0: all of them): the label
-    with thousands of tokens crosses many chunks of the one-hot dW sum.  dW matches the
-    oracle and is the same bit for bit on a second run."""
+    """A token distribution where one id fills most positions (1.0: all of them): one dW row
+    sums the one-hot terms of thousands of tokens (through the exp-logit operand).  dW matches
+    the oracle and is the same bit for bit on a second run."""
     pb = Problem(3, DEV, Q=8, len_range=(60, 200), V=500, d=64, skew=skew)
     ref = pb.oracle_loss()
     st = _status()
