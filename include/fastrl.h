@@ -277,7 +277,10 @@ int64_t fastrl_token_logprob_noalloc_max_chunk(int32_t V);
  *   (ceil(left / slab_tokens) slabs to go, recounted after every slab) and never holds more
  *   than max(1.25 slab_tokens, longest sequence) tokens.  Each slab stores exp(z - s_t)
  *   (s_t = 0, or the row max when exp(z) would leave float range) for its tokens in the
- *   workspace, so the [T, V] logits are never stored: the workspace holds
+ *   workspace, with each token's label entry lowered by exp(lse_t - s_t) so that the two
+ *   backward contractions over it yield the whole of dZ, one-hot term included (that term
+ *   thus carries one rounding to the operand's type: at most 2^-8 |g_t| per token in bf16,
+ *   as with a bf16 dlogits operand).  The [T, V] logits are never stored: the workspace holds
  *   slab * V_pad * sizeof(dtype) bytes (V_pad = V rounded up to 256; 10 GB for the default
  *   slab at V = 152064 in bf16), W^T (d * V_pad) when dhidden is wanted, and small per-token
  *   and per-(vocabulary block, token) arrays.
