@@ -209,6 +209,28 @@ def extra_rows(cfg, ro, inp, fr, max_group, max_len, last, args):
     dev = inp["H"].device
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
     rows = {}
+    # the step's small stages on the workload's own rewards: advantage (A1), and pruning with
+    # the compaction of the kept tokens (A2 + A3); algorithmic bytes: A1 reads the rewards and
+    # group offsets and writes advantage, class and validity; A2 + A3 read every token id once,
+    # write and read back one 8-byte n-gram key per token, and write the kept-token index
+    N, Q, Tt = len(ro.rewards), len(ro.group_off) - 1, int(ro.T_total)
+    a_ms = _time_gpu(lambda: fr.advantage(inp["rewards"], inp["group_off"],
+                                          drop_uniform=cfg.drop_uniform), 50)
+    adv0, cls0, valid0 = fr.advantage(inp["rewards"], inp["group_off"],
+                                      drop_uniform=cfg.drop_uniform)
+    p_ms = _time_gpu(lambda: fr.prune(inp["token_ids"], inp["traj_tok_off"], inp["rewards"],
+                                      inp["group_off"], cls0, valid0, V=cfg.V,
+                                      max_group=max_group, max_len=max_len,
+                                      keep_ratio=cfg.keep_ratio), 20)
+    a_bytes = 4 * N + 4 * (Q + 1) + 4 * N + 4 * N + Q
+    p_bytes = 4 * Tt + 16 * Tt + 4 * last["t_kept"] + 8 * (N + 1)
+    rows["small_stages"] = dict(
+        advantage_us=a_ms * 1e3, advantage_bytes=a_bytes,
+        advantage_GBps=a_bytes / (a_ms * 1e-3) / 1e9,
+        prune_compact_us=p_ms * 1e3, prune_compact_bytes=p_bytes,
+        prune_compact_GBps=p_bytes / (p_ms * 1e-3) / 1e9, hbm_peak_GBps=8000.0,
+        note="latency-bound: a few launches over KB to a few MB (the loss kernel is timed "
+             "inside the loss call; see the kernel trace)")
     # N1: continuous groups |A_i - A_j| < 1e-4 (continuous rewards of the same batch shape)
     rw = continuous_rewards(ro.group_off, seed=cfg.seed)
     rw_d = t(rw)

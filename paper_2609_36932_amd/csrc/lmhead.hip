@@ -102,6 +102,7 @@ struct GemmParams {
   int32_t Vreal;
   int32_t store_e;          // 0: partials only, 1: partials + E, 2: same for redo blocks
   const int32_t* redo_blk;  // [nnb] token blocks to evaluate again (store_e == 2)
+  const int32_t* redo_any;  // nonzero iff some token block of the slab is marked
   // ---- DH epilogue
   void* dH;                 // [.., d] at slab offset
   int32_t dH_bf16;
@@ -1050,6 +1051,30 @@ void lm_bwd_kernel(const GemmParams q, const GemmParams r) {
   }
 }
 
+// Second evaluation of the bf16 logits tiles whose token block holds a row that needs a shift:
+// at most one block per compute unit walks the tiles in grid order and evaluates those of marked
+// token blocks (store_e == 2); with no row marked, the usual case, every block returns at once.
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void lm_redo_kernel(const GemmParams p) {
+  if (p.redo_any[0] == 0) return;
+  __shared__ __attribute__((aligned(16))) char smem_raw[SmemBytes<uint16_t>::value];
+  uint16_t* smem = reinterpret_cast<uint16_t*>(smem_raw);
+  const int nt = p.nmb * p.nnb;
+  for (int b = blockIdx.x; b < nt; b += gridDim.x) {
+    int mb, nb;
+    tile_coords<MODE_FWD>(mb, nb, p.nmb, p.nnb, b);
+    if (p.redo_blk[nb] == 0) continue;  // the same for the whole block
+    f32x4_t acc[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    mainloop_bf16_dma<MODE_FWD>(p, mb * kBM, nb * kBN, acc, smem);
+    fwd_epilogue_bf16(p, mb * kBM, nb * kBN, mb, acc, smem);
+    __syncthreads();  // the epilogue's LDS exchange is read before the next tile's loads land
+  }
+}
+
 // ------------------------------------------------------------------ small kernels
 
 // s_t = 0, labels of the slab, validity
@@ -1081,7 +1106,10 @@ __global__ __launch_bounds__(256) void merge_kernel(
     const float* __restrict__ psz, int64_t ldp, int32_t nmb, const float* __restrict__ zlab,
     const int32_t* __restrict__ yslab, int32_t Tc, int32_t rel, int32_t check,
     float* __restrict__ lse_out, float* __restrict__ logp_out, float* __restrict__ ent_out,
-    float* __restrict__ shift, int32_t* __restrict__ redo_blk, int32_t* __restrict__ redo_count) {
+    float* __restrict__ shift, int32_t* __restrict__ redo_blk, int32_t* __restrict__ redo_count,
+    int32_t* __restrict__ redo_any, int32_t only_after_redo) {
+  // the second merge only matters when the first marked a row (every block reads the same flag)
+  if (only_after_redo && redo_any[0] == 0) return;
   __shared__ float sm[4][64], ss[4][64], sz[4][64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int t = blockIdx.x * 64 + lane;
@@ -1143,6 +1171,7 @@ __global__ __launch_bounds__(256) void merge_kernel(
   if (rel && check && !(Mt - s_t < 60.0f && Mt - s_t > -60.0f)) {
     shift[t] = Mt;
     redo_blk[t / kBN] = 1;
+    redo_any[0] = 1;
     atomicAdd(redo_count, 1);
   }
 }
@@ -1401,6 +1430,21 @@ static int launch_bwd(GemmParams q, GemmParams r, double flops, hipStream_t stre
   return FASTRL_OK;
 }
 
+// the second evaluation of marked token blocks (store_e == 2): bf16 through lm_redo_kernel
+template <typename T>
+static int launch_redo(GemmParams p, hipStream_t stream) {
+  p.store_e = 2;
+  if constexpr (sizeof(T) != 2) return launch_gemm<T, MODE_FWD>(p, -1, 0.0, stream);
+  p.nmb = int((p.M + kBM - 1) / kBM);
+  p.nnb = int((p.N + kBN - 1) / kBN);
+  const int64_t nblk = int64_t(p.nmb) * p.nnb;
+  if (nblk == 0) return FASTRL_OK;
+  hipLaunchKernelGGL(lm_redo_kernel, dim3(unsigned(std::min<int64_t>(nblk, 256))), dim3(512), 0,
+                     stream, p);
+  FR_LAUNCHED();
+  return FASTRL_OK;
+}
+
 #define FR_TRY(x)                 \
   do {                            \
     int rc_ = (x);                \
@@ -1468,7 +1512,8 @@ static int token_logprob_impl(const void* hidden, const int32_t* row_index, cons
     hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 64)), dim3(256), 0, stream, w.pmax, w.psum,
                        (const float*)nullptr, ch, nmb, w.zlab, w.yslab, Tc, 0, 0,
                        lse ? lse + t0 : (float*)nullptr, logp + t0, (float*)nullptr,
-                       (float*)nullptr, (int32_t*)nullptr, (int32_t*)nullptr);
+                       (float*)nullptr, (int32_t*)nullptr, (int32_t*)nullptr,
+                       (int32_t*)nullptr, 0);
     FR_LAUNCHED();
   }
   return FASTRL_OK;
@@ -1622,7 +1667,7 @@ static size_t carve_loss(Carver& c, LossWs& w, const fastrl_loss_args& a, int64_
   w.shift = c.take<float>(size_t(tcp));
   w.cslab = c.take<float>(size_t(tcp));
   w.yslab = c.take<int32_t>(size_t(tcp));
-  w.redo_blk = c.take<int32_t>(size_t(tcp / kBN));
+  w.redo_blk = c.take<int32_t>(size_t(tcp / kBN + 1));  // + the slab's any-marked flag
   w.redo_count = c.take<int32_t>(1);
   w.lse = a.lse ? a.lse : c.take<float>(size_t(std::max<int64_t>(a.T, 1)));
   w.logp = a.logp ? a.logp : c.take<float>(size_t(std::max<int64_t>(a.T, 1)));
@@ -1701,7 +1746,7 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
                        a.token_ids, a.row_index, t0, Tc, V, w.yslab, w.shift, a.status);
     FR_LAUNCHED();
     hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(256), 0, stream, w.redo_blk,
-                       int64_t(nnb), 0);
+                       int64_t(nnb) + 1, 0);
     FR_LAUNCHED();
     GemmParams p{};
     p.A = a.W; p.lda = d; p.M = V;
@@ -1711,22 +1756,24 @@ static int policy_loss_impl(const fastrl_loss_args& a, hipStream_t stream) {
     p.yslab = w.yslab; p.shift = w.shift; p.E1 = w.E1; p.ldE1 = Vpad;
     p.Vreal = V; p.store_e = (dh || dw) ? 1 : 0; p.status = a.status;
     p.redo_blk = w.redo_blk;
+    p.redo_any = w.redo_blk + nnb;
     const double f_fwd = 2.0 * double(V) * Tc * d;
     FR_TRY((launch_gemm<T, MODE_FWD>(p, FASTRL_K_LOGITS_FWD, f_fwd, stream)));
     const bool store = dh || dw;
     hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 64)), dim3(256), 0, stream,
                        w.pmax, w.psum, w.psz, tcp, nmb, w.zlab, w.yslab, Tc, store ? 1 : 0,
                        store ? 1 : 0, w.lse + t0, w.logp + t0, w.ent ? w.ent + t0 : nullptr,
-                       store ? w.shift : (float*)nullptr, w.redo_blk, w.redo_count);
+                       store ? w.shift : (float*)nullptr, w.redo_blk, w.redo_count,
+                       w.redo_blk + nnb, 0);
     FR_LAUNCHED();
     if (store) {
-      // token blocks holding a row that needs a shift: evaluate again, then merge again
-      p.store_e = 2;
-      FR_TRY((launch_gemm<T, MODE_FWD>(p, -1, 0.0, stream)));
+      // token blocks holding a row that needs a shift: evaluate again, then merge again (both
+      // return at once on the device when no row was marked)
+      FR_TRY(launch_redo<T>(p, stream));
       hipLaunchKernelGGL(merge_kernel, dim3(nb1d(Tc, 64)), dim3(256), 0, stream,
                          w.pmax, w.psum, w.psz, tcp, nmb, w.zlab, w.yslab, Tc, 1, 0, w.lse + t0,
                          w.logp + t0, w.ent ? w.ent + t0 : nullptr, w.shift, w.redo_blk,
-                         w.redo_count);
+                         w.redo_count, w.redo_blk + nnb, 1);
       FR_LAUNCHED();
     }
     hipLaunchKernelGGL(loss_kernel, dim3(unsigned(s1 - s0)), dim3(256), 0, stream, w.logp,
