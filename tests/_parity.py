@@ -89,6 +89,29 @@ class Problem:
         Hp[torch.from_numpy(pruned)] = float("nan")
         self.H_poisoned = Hp
 
+    def scale_hidden(self, rows, factor):
+        """Multiply the hidden rows `rows` (indices into the full batch) by `factor` (a power of
+        two, exact in bf16) and redo everything built from H: the oracle's log-probs and
+        log-sum-exps of the kept tokens, the old / ref log-probs, the poisoned copy."""
+        H = self.H.clone()
+        H[torch.as_tensor(rows, dtype=torch.long)] *= factor
+        self.H = H
+        self.H64 = H.double().numpy()
+        lp, lse = oracle.token_logprob(self.H64[self.src], self.W64, self.y)
+        self.logp_exact, self.lse_exact = lp, lse
+        ro = self.ro
+        old = np.full(ro.T_total, np.nan)
+        ref = np.full(ro.T_total, np.nan)
+        old[self.src] = lp + ro.old_noise[self.src]
+        ref[self.src] = lp + ro.ref_noise[self.src]
+        self.old = old.astype(np.float32)
+        self.ref = ref.astype(np.float32)
+        Hp = H.clone()
+        pruned = np.ones(ro.T_total, dtype=bool)
+        pruned[self.src] = False
+        Hp[torch.from_numpy(pruned)] = float("nan")
+        self.H_poisoned = Hp
+
     def oracle_loss(self):
         base = self.cfg
         kept = self.pr["kept_traj"]

@@ -211,6 +211,36 @@ def test_large_logits_take_the_shifted_path(fr):
                 dg=ref["dg"], lse=pb.lse_exact)
 
 
+def test_shifted_path_in_some_slabs(fr):
+    """Slabs of ~80 tokens where only the rows of every third kept sequence have logits of
+    magnitude ~100 (their hidden rows scaled by 32): exactly those slabs re-evaluate their
+    marked token blocks (each slab's flag starts cleared; slabs without a marked row skip the
+    second evaluation and merge), and every slab matches the oracle."""
+    pb = Problem(3, DEV, Q=4, len_range=(20, 60), V=700, d=64, w_std=0.2)
+    koff = pb.pr["kept_tok_off"]
+    big = np.concatenate([pb.src[koff[i]:koff[i + 1]] for i in range(0, len(koff) - 1, 3)])
+    pb.scale_hidden(big, 32.0)
+    ref = pb.oracle_loss()
+    st = _status()
+    out = pb.run_gpu(fr, slab_tokens=80, status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0, fr.status_names(st.item())
+    call = out["call"]
+    T = out["t_kept"]
+    nslab = len(call.slab_plan()[0]) - 1
+    n_big = len(big)
+    # every scaled row (|max logit| >= 106) is marked, no other row (|max logit| < 8)
+    assert nslab >= 4 and int(call.stats[1].item()) == n_big, (nslab, call.stats[1].item(), n_big)
+    err = np.abs(call.logp[:T].double().cpu().numpy() - pb.logp_exact).max()
+    err_lse = np.abs(call.lse[:T].double().cpu().numpy() - pb.lse_exact).max()
+    assert err < LOGP_ATOL and err_lse < LOGP_ATOL, (err, err_lse)
+    assert abs(call.loss.item() - ref["loss"]) <= REL * max(abs(ref["loss"]), 1e-12)
+    assert int(call.stats[0].item()) == ref["clipped"]
+    check_grads(pb.H64[pb.src], pb.W64, pb.y, ref["g"], call.dhidden[:T].double().cpu().numpy(),
+                call.dW.double().cpu().numpy(), ref["dH"], ref["dW"],
+                dg=ref["dg"], lse=pb.lse_exact)
+
+
 @pytest.mark.parametrize("slab", [0, 120])
 def test_deterministic(fr, slab):
     """Two runs give the same bits: masks and offsets, the loss, dhidden and dW (with several
