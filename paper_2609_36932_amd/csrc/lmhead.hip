@@ -89,6 +89,7 @@ struct GemmParams {
   int64_t b_row_base;       // FWD: first kept token of the slab
   int32_t K;
   int32_t nmb, nnb;         // block grid (M blocks, N blocks)
+  int32_t group;            // tile order: M-blocks per sweep over the N-blocks (tile_group)
   // ---- FWD epilogue
   float* pmax;              // [nmb][ldp]
   float* psum;              // [nmb][ldp]
@@ -115,26 +116,25 @@ struct GemmParams {
 };
 
 // Tile order: consecutive blocks are dealt round-robin to the 8 XCDs and run at about the same
-// time, so the order of logical tiles decides which operand strips are in use together.  GROUP
-// M-blocks share each sweep over the N-blocks.  Logits GEMM (short K): 32, so each XCD holds 4
-// vocab blocks x 8 token blocks of the 256 tiles in flight and all XCDs read the same 8 hidden
-// row blocks.  Backward GEMMs (long K): 4; all XCDs walk neighbouring tiles through K together,
+// time, so the order of logical tiles decides which operand strips are in use together.  A group
+// of M-blocks shares each sweep over the N-blocks (p.group, chosen per shape on the host by
+// tile_group).  Logits GEMM (short K): 32 at d = 3584, so each XCD holds 4 vocab blocks x 8
+// token blocks of the 256 tiles in flight and all XCDs read the same 8 hidden row blocks.
+// Backward GEMMs (long K): 4 at d = 3584; all XCDs walk neighbouring tiles through K together,
 // so a strip that several XCDs read is fetched once into the shared last-level cache (giving
 // each XCD its own contiguous range of tiles measured 2-4% slower here).
-constexpr int kGroupFwd = 32, kGroupDh = 4, kGroupDw = 4;
 // spins of a split-barrier wait before it gives up (each spin one LDS read, ~0.1 us; a
 // wavefront normally waits for a few hundred cycles at most)
 constexpr int kSyncSpins = 1 << 16;
 template <int MODE>
-__device__ __forceinline__ void tile_coords(int& mb, int& nb, int nmb, int nnb, int b) {
-  constexpr int GROUP = MODE == MODE_FWD ? kGroupFwd : MODE == MODE_DH ? kGroupDh : kGroupDw;
+__device__ __forceinline__ void tile_coords(int& mb, int& nb, int nmb, int nnb, int b, int group) {
   // the groups are vocab blocks in both dW forms: M blocks of MODE_DW, N blocks of MODE_DWT
   constexpr bool GN = MODE == MODE_DWT;
   const int ng = GN ? nnb : nmb, ns = GN ? nmb : nnb;
-  const int per_group = GROUP * ns;
+  const int per_group = group * ns;
   const int gid = b / per_group;
-  const int first = gid * GROUP;
-  const int gsz = min(ng - first, GROUP);
+  const int first = gid * group;
+  const int gsz = min(ng - first, group);
   const int in = b % per_group;
   const int a = first + in % gsz, sweep = in / gsz;
   mb = GN ? sweep : a;
@@ -831,7 +831,7 @@ void lm_gemm_kernel(const GemmParams p) {
   __shared__ __attribute__((aligned(16))) char smem_raw[SmemBytes<T>::value];
   T* smem = reinterpret_cast<T*>(smem_raw);
   int mb, nb;
-  tile_coords<MODE>(mb, nb, p.nmb, p.nnb, blockIdx.x);
+  tile_coords<MODE>(mb, nb, p.nmb, p.nnb, blockIdx.x, p.group);
   if (MODE == MODE_FWD && p.store_e == 2 && p.redo_blk[nb] == 0) return;
   const int m0 = mb * kBM, n0 = nb * kBN;
   constexpr int NI = Geo<T, MODE>::NI, NT = Geo<T, MODE>::THREADS;
@@ -1041,11 +1041,11 @@ void lm_bwd_kernel(const GemmParams q, const GemmParams r) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
   if (b < nh) {
-    tile_coords<MODE_DH>(mb, nb, q.nmb, q.nnb, b);
+    tile_coords<MODE_DH>(mb, nb, q.nmb, q.nnb, b, q.group);
     mainloop_bf16_dma<MODE_DH>(q, mb * kBM, nb * kBN, acc, smem);
     dh_epilogue_bf16(q, mb * kBM, nb * kBN, acc);
   } else {
-    tile_coords<MODE_DWT>(mb, nb, r.nmb, r.nnb, b - nh);
+    tile_coords<MODE_DWT>(mb, nb, r.nmb, r.nnb, b - nh, r.group);
     mainloop_bf16_dma<MODE_DWT>(r, mb * kBM, nb * kBN, acc, smem);
     dwt_epilogue_bf16(r, mb * kBM, nb * kBN, acc);
   }
@@ -1062,7 +1062,7 @@ void lm_redo_kernel(const GemmParams p) {
   const int nt = p.nmb * p.nnb;
   for (int b = blockIdx.x; b < nt; b += gridDim.x) {
     int mb, nb;
-    tile_coords<MODE_FWD>(mb, nb, p.nmb, p.nnb, b);
+    tile_coords<MODE_FWD>(mb, nb, p.nmb, p.nnb, b, p.group);
     if (p.redo_blk[nb] == 0) continue;  // the same for the whole block
     f32x4_t acc[8][4];
 #pragma unroll
@@ -1391,10 +1391,22 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
 
 static inline int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
+// Tile group of a GEMM (tile_coords), measured back to back on the two hidden sizes of the
+// workloads: the logits GEMM takes 32 at K = d = 3584 (8 and 16 lose 5% and 2.5% there, 64 is
+// level) and 16 at d = 1536 (+5% on that GEMM against 32; 8, 12, 20, 24 and 64 are slower
+// too); dhidden 4 when d spans 14 column blocks (2, 8 and 16 lose ~1.5%) and 8 when it spans 6
+// (+2% on the backward launch at d = 1536); the dW tiles 4 at both (2 and 8 lose).
+static int tile_group(int mode, int32_t K, int32_t nnb) {
+  if (mode == MODE_FWD) return K <= 2048 ? 16 : 32;
+  if (mode == MODE_DH) return nnb <= 8 ? 8 : 4;
+  return 4;
+}
+
 template <typename T, int MODE>
 static int launch_gemm(GemmParams p, int kind, double flops, hipStream_t stream) {
   p.nmb = int((p.M + kBM - 1) / kBM);
   p.nnb = int((p.N + kBN - 1) / kBN);
+  p.group = tile_group(MODE, p.K, p.nnb);
   const int64_t nblk = int64_t(p.nmb) * p.nnb;
   if (nblk == 0) return FASTRL_OK;
   FR_CHECK_ARG(sizeof(T) != 2 || MODE != MODE_DW ||
@@ -1418,6 +1430,8 @@ static int launch_bwd(GemmParams q, GemmParams r, double flops, hipStream_t stre
   q.nnb = int((q.N + kBN - 1) / kBN);
   r.nmb = int((r.M + kBM - 1) / kBM);
   r.nnb = int((r.N + kBN - 1) / kBN);
+  q.group = tile_group(MODE_DH, q.K, q.nnb);
+  r.group = tile_group(MODE_DWT, r.K, r.nnb);
   const int64_t nh = int64_t(q.nmb) * q.nnb, nw = int64_t(r.nmb) * r.nnb;
   if (nh + nw == 0) return FASTRL_OK;
   FR_CHECK_ARG(nh + nw < (int64_t(1) << 31), FASTRL_ERR_UNSUPPORTED, "backward GEMMs: grid too large");
@@ -1437,6 +1451,7 @@ static int launch_redo(GemmParams p, hipStream_t stream) {
   if constexpr (sizeof(T) != 2) return launch_gemm<T, MODE_FWD>(p, -1, 0.0, stream);
   p.nmb = int((p.M + kBM - 1) / kBM);
   p.nnb = int((p.N + kBN - 1) / kBN);
+  p.group = tile_group(MODE_FWD, p.K, p.nnb);
   const int64_t nblk = int64_t(p.nmb) * p.nnb;
   if (nblk == 0) return FASTRL_OK;
   hipLaunchKernelGGL(lm_redo_kernel, dim3(unsigned(std::min<int64_t>(nblk, 256))), dim3(512), 0,
