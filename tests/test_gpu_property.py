@@ -135,3 +135,51 @@ def test_loss_properties(fr, case):
     dg = g_deviation(x, o, f if beta else None, off, A, **kw)
     check_grads(H64[:T], W64, y[:T], g, call.dhidden[:T].double().cpu().numpy(),
                 call.dW.double().cpu().numpy(), dH, dW, dg=dg, lse=lse)
+
+
+@st.composite
+def logprob_cases(draw):
+    rows = draw(st.integers(1, 300))
+    T = draw(st.integers(0, 400))
+    V = draw(st.sampled_from([1, 2, 7, 255, 256, 257, 1000, 2600]))
+    d = draw(st.sampled_from([8, 64, 136, 264]))
+    dtype = draw(st.sampled_from(["bf16", "f32"]))
+    gather = draw(st.booleans())
+    scale = draw(st.sampled_from([1.0, 30.0]))
+    seed = draw(st.integers(0, 2**31 - 1))
+    return rows, T, V, d, dtype, gather, scale, seed
+
+
+@SETTINGS
+@given(logprob_cases())
+def test_token_logprob_properties(fr, case):
+    """fastrl_token_logprob and fastrl_token_logprob_noalloc on random shapes: vocabularies
+    from 1 to 2600 (ragged last vocabulary block), hidden sizes 8 to 264, gathered rows with
+    repeats or the first T rows, both dtypes, logits of magnitude ~1 or ~100; log-probs and
+    log-sum-exps against the oracle, the two entry points identical."""
+    rows, T, V, d, dtype, gather, scale, seed = case
+    if not gather:
+        T = min(T, rows)
+    rng = np.random.default_rng(seed)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    H = torch.from_numpy(rng.normal(0, scale, size=(rows, d)).astype(np.float32)).to(tdt)
+    W = torch.from_numpy(rng.normal(0, 0.05, size=(V, d)).astype(np.float32)).to(tdt)
+    y = rng.integers(0, V, size=rows).astype(np.int32)
+    idx = rng.integers(0, rows, size=T).astype(np.int32) if gather else np.arange(T, dtype=np.int32)
+    H64, W64 = H.double().numpy(), W.double().numpy()
+    lp_ref, lse_ref = oracle.token_logprob(H64[idx], W64, y[idx].astype(np.int64))
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    st_ = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ri = t(idx) if gather else None
+    lp, lse = fr.token_logprob(H.to(DEV), W.to(DEV), t(y), row_index=ri, T=T, status=st_)
+    lp2 = torch.full((max(T, 1),), float("nan"), device=DEV)
+    lse2 = torch.full((max(T, 1),), float("nan"), device=DEV)
+    fr.token_logprob_noalloc(H.to(DEV), W.to(DEV), t(y), lp2, lse2, row_index=ri, T=T,
+                             status=st_)
+    torch.cuda.synchronize()
+    assert st_.item() == 0, fr.status_names(st_.item())
+    if T == 0:
+        return
+    assert np.abs(lp.double().cpu().numpy() - lp_ref).max() < LOGP_ATOL
+    assert np.abs(lse.double().cpu().numpy() - lse_ref).max() < LOGP_ATOL
+    assert torch.equal(lp, lp2[:T]) and torch.equal(lse, lse2[:T])
